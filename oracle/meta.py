@@ -1,0 +1,152 @@
+"""Varlen-metadata twin and work-list checker.
+
+A mixed iteration packs the decoders' single query tokens and the prefill
+chunk's ``p_t`` tokens into one batch (``D_t`` and ``p_t`` of Eq. 1, Sec. 2.1).
+Its metadata has exactly one correct value, written out here with plain loops:
+
+* ``cu_q[s]``        exclusive prefix sum of the per-sequence query counts;
+* ``q_pos0[s]``      absolute position of sequence ``s``'s first new token,
+                     ``kv_len[s] - q_len[s]``;
+* ``slot_mapping``   for every new token, in packed order, the flat pool slot
+                     ``block_table[s][pos // 16] * 16 + pos % 16`` it is written
+                     to (PagedAttention block addressing, Sec. 2.1).
+
+The work list (how the attention launch splits the iteration into units) has
+many valid values, so it is not recomputed; ``check_work_list`` verifies the
+properties any valid list must have.
+"""
+from __future__ import annotations
+
+from typing import Dict, List, Sequence, Tuple
+
+import numpy as np
+
+PAGE = 16
+HEAD_DIM = 128
+TILE_ROWS = 128          # query rows (tokens x grouped heads) one prefill unit holds
+
+# Work-item field indices (16 int32 per unit).
+W_SEQ, W_KVHEAD, W_QTOK0, W_QNTOK, W_KVBEGIN, W_KVEND = 0, 1, 2, 3, 4, 5
+W_GROUP, W_SPLIT, W_NSPLITS, W_WSOFF, W_WSGROUP, W_KIND = 6, 7, 8, 9, 10, 11
+WORK_INTS = 16
+KIND_PREFILL, KIND_DECODE = 0, 1
+
+
+def varlen_meta(q_len: Sequence[int], kv_len: Sequence[int], block_table: np.ndarray
+                ) -> Tuple[List[int], List[int], List[int]]:
+    """Return (cu_q, q_pos0, slot_mapping) as Python int lists."""
+    cu_q = [0]
+    q_pos0 = []
+    slots = []
+    for s in range(len(q_len)):
+        cu_q.append(cu_q[-1] + int(q_len[s]))
+        first = int(kv_len[s]) - int(q_len[s])
+        q_pos0.append(first)
+        for pos in range(first, int(kv_len[s])):
+            block = int(block_table[s][pos // PAGE])
+            slots.append(block * PAGE + pos % PAGE)
+    return cu_q, q_pos0, slots
+
+
+class WorkListError(AssertionError):
+    pass
+
+
+def check_work_list(work: np.ndarray, num_prefill: int, q_len: Sequence[int],
+                    kv_len: Sequence[int], num_q_heads: int, num_kv_heads: int,
+                    num_groups: int, workspace_bytes: int) -> Dict[str, int]:
+    """Raise ``WorkListError`` unless ``work`` is a valid unit list for the iteration.
+
+    Validity: every visible (query token, key) pair of every (sequence, KV head)
+    is covered by exactly one unit; units respect sequence bounds and page
+    alignment; prefill units precede decode units; a unit is a decode unit iff
+    its sequence has a single new token; split groups are complete and ordered;
+    partial-result slots are disjoint and inside the workspace.
+    """
+    def fail(msg):
+        raise WorkListError(msg)
+
+    g = num_q_heads // num_kv_heads
+    n_seq = len(q_len)
+    work = np.asarray(work, dtype=np.int64).reshape(-1, WORK_INTS)
+    counts = {}
+    groups: Dict[int, List[np.ndarray]] = {}
+    partial_base = ((num_groups * 4 + 255) // 256 * 256) // 4
+    slots = []
+    for u, it in enumerate(work):
+        s, kh, t0, nt, kb, ke = (int(x) for x in it[:6])
+        grp, split, nsp, wsoff, wsgrp, kind = (int(x) for x in it[6:12])
+        if not (0 <= s < n_seq and 0 <= kh < num_kv_heads):
+            fail(f"unit {u}: bad seq/head")
+        ql, kl = int(q_len[s]), int(kv_len[s])
+        pos0 = kl - ql
+        if not (0 <= t0 and nt >= 1 and t0 + nt <= ql):
+            fail(f"unit {u}: query rows out of range")
+        if not (0 <= kb < ke <= kl) or kb % PAGE:
+            fail(f"unit {u}: key range [{kb},{ke}) invalid for kv_len {kl}")
+        if ke > pos0 + t0 + nt:
+            fail(f"unit {u}: keys beyond the last row's position")
+        want_kind = KIND_DECODE if ql == 1 else KIND_PREFILL
+        if kind != want_kind:
+            fail(f"unit {u}: kind {kind} but q_len {ql}")
+        if (kind == KIND_PREFILL) != (u < num_prefill):
+            fail(f"unit {u}: prefill units must come first")
+        if kind == KIND_PREFILL and nt * g > TILE_ROWS:
+            fail(f"unit {u}: {nt}x{g} rows exceed a tile")
+        # at least one visible pair: first key visible to the last row
+        if kb > pos0 + t0 + nt - 1:
+            fail(f"unit {u}: no visible key")
+        key = (s, kh)
+        if key not in counts:
+            counts[key] = np.zeros((ql, kl), dtype=np.int32)
+        counts[key][t0:t0 + nt, kb:ke] += 1
+        if nsp < 1 or not (0 <= split < nsp):
+            fail(f"unit {u}: bad split {split}/{nsp}")
+        if nsp == 1:
+            if grp != -1:
+                fail(f"unit {u}: single split must have group -1")
+        else:
+            if not (0 <= grp < num_groups):
+                fail(f"unit {u}: group {grp} out of range")
+            groups.setdefault(grp, []).append(it)
+            rows = nt * g
+            slot_floats = rows * (HEAD_DIM + 2)
+            if wsoff != wsgrp + split * slot_floats:
+                fail(f"unit {u}: partial slot offset")
+            if wsgrp < partial_base:
+                fail(f"unit {u}: partial slot overlaps counters")
+            slots.append((wsoff, wsoff + slot_floats))
+    for (s, kh), c in counts.items():
+        ql, kl = int(q_len[s]), int(kv_len[s])
+        pos0 = kl - ql
+        vis = np.arange(kl)[None, :] <= (pos0 + np.arange(ql))[:, None]
+        if np.any(c[vis] != 1):
+            fail(f"seq {s} head {kh}: visible pairs not covered exactly once")
+    for s in range(n_seq):
+        for kh in range(num_kv_heads):
+            if (s, kh) not in counts and int(q_len[s]) > 0:
+                fail(f"seq {s} head {kh}: no unit")
+    for grp, its in groups.items():
+        nsp = int(its[0][W_NSPLITS])
+        if len(its) != nsp:
+            fail(f"group {grp}: {len(its)} units for {nsp} splits")
+        ref = its[0]
+        for it in its:
+            if any(int(it[f]) != int(ref[f]) for f in (W_SEQ, W_KVHEAD, W_QTOK0, W_QNTOK,
+                                                     W_NSPLITS, W_WSGROUP)):
+                fail(f"group {grp}: units disagree on rows")
+        by_split = sorted(its, key=lambda it: int(it[W_SPLIT]))
+        if [int(it[W_SPLIT]) for it in by_split] != list(range(nsp)):
+            fail(f"group {grp}: split indices")
+        for a, b in zip(by_split, by_split[1:]):
+            if int(a[W_KVEND]) != int(b[W_KVBEGIN]):
+                fail(f"group {grp}: split ranges not contiguous and ordered")
+    slots.sort()
+    for (a0, a1), (b0, b1) in zip(slots, slots[1:]):
+        if b0 < a1:
+            fail("partial slots overlap")
+    if slots and slots[-1][1] * 4 > workspace_bytes:
+        fail("partial slots exceed the workspace")
+    if num_groups * 4 > workspace_bytes and num_groups:
+        fail("counters exceed the workspace")
+    return {"units": len(work), "groups": len(groups)}

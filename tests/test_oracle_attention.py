@@ -1,0 +1,119 @@
+"""Oracle attention pinned against brute force, closed forms, a library routine and invariants."""
+import numpy as np
+import pytest
+
+from oracle import attention as oa
+from oracle import paging
+from paper_2609_38386_amd import workload as wl
+
+from _attention_pins import (check_brute_force, check_chunking_invariance, check_closed_forms,
+                             check_decode_equals_last_prefill_row, check_large_scores,
+                             check_library_sdpa)
+
+
+def test_brute_force():
+    check_brute_force(oa.attention_sequence)
+
+
+def test_large_scores_need_max_subtraction():
+    check_large_scores(oa.attention_sequence)
+
+
+def test_closed_forms():
+    check_closed_forms(oa.attention_sequence)
+
+
+def test_library_sdpa_gqa_as_repeated_mha():
+    check_library_sdpa(oa.attention_sequence)
+
+
+def test_chunking_invariance():
+    check_chunking_invariance(oa.attention_sequence)
+
+
+def test_decode_row_equals_last_prefill_row():
+    check_decode_equals_last_prefill_row(oa.attention_sequence)
+
+
+def test_row_subset_matches_full():
+    rng = np.random.default_rng(3)
+    q = rng.standard_normal((9, 4, 128))
+    k = rng.standard_normal((30, 2, 128))
+    v = rng.standard_normal((30, 2, 128))
+    full = oa.attention_sequence(q, k, v, 0.1)
+    sub = oa.attention_sequence(q, k, v, 0.1, rows=[0, 4, 8])
+    assert np.allclose(sub, full[[0, 4, 8]], rtol=0, atol=1e-13)
+
+
+def test_bf16_widening_exact():
+    bits = np.array([0x3F80, 0xBF80, 0x4049, 0x0000, 0x8000, 0x7F7F, 0x0001], dtype=np.uint16)
+    got = oa.bf16_bits_to_float64(bits)
+    assert got[0] == 1.0 and got[1] == -1.0 and got[3] == 0.0
+    assert got[2] == 3.140625
+    assert np.signbit(got[4])
+    assert got[5] == float.fromhex("0x1.fep127")
+    assert got[6] == float.fromhex("0x1p-133")
+
+
+def _scatter(logical_k, logical_v, block_row, pool_blocks):
+    """Test-side writer of the pool layout (token rows for K, transposed pages for V)."""
+    n, hkv, d = logical_k.shape
+    kc = np.zeros((pool_blocks, hkv, 16, d), dtype=np.uint16)
+    vc = np.zeros((pool_blocks, hkv, d, 16), dtype=np.uint16)
+    for j in range(n):
+        b = block_row[j // 16]
+        kc[b, :, j % 16, :] = logical_k[j]
+        vc[b, :, :, j % 16] = logical_v[j]
+    return kc, vc
+
+
+def test_gather_hand_example():
+    """Element (block b, head h, slot t, dim d) holds 1000b + 100h + t for K (and + 50 for V)."""
+    nb, hkv, d = 4, 2, 3
+    kc = np.zeros((nb, hkv, 16, d), dtype=np.uint16)
+    vc = np.zeros((nb, hkv, d, 16), dtype=np.uint16)
+    for b in range(nb):
+        for h in range(hkv):
+            for t in range(16):
+                kc[b, h, t, :] = 1000 * b + 100 * h + t
+                vc[b, h, :, t] = 1000 * b + 100 * h + t + 50
+    k, v = paging.gather_sequence(kc, vc, np.array([3, 1]), 20)
+    # token 0 -> block 3 slot 0; token 15 -> block 3 slot 15; token 17 -> block 1 slot 1
+    assert k[0, 0, 0] == 3000 and k[15, 1, 2] == 3115 and k[17, 0, 1] == 1001
+    assert v[17, 1, 0] == 1151 and v[19, 0, 2] == 1053
+
+
+def test_page_permutation_invariance():
+    """Two different physical placements gather to the same bits, hence the same outputs."""
+    shape = wl.AttnShape(4, 2)
+    st = wl.SeqStream(5, wl.ROLE_DECODER, 0, shape, 53)
+    outs = []
+    for seed in (1, 2):
+        bt = wl.block_tables(seed, [wl.pages_for(53)], 16)[0]
+        kc, vc = _scatter(st.k, st.v, bt, 16)
+        k, v = paging.gather_sequence(kc, vc, bt, 53)
+        assert np.array_equal(k, st.k) and np.array_equal(v, st.v)
+        outs.append(oa.attention_sequence(oa.bf16_bits_to_float64(st.q[-7:]),
+                                          oa.bf16_bits_to_float64(k),
+                                          oa.bf16_bits_to_float64(v), 0.088))
+    assert np.array_equal(outs[0], outs[1])
+
+
+def test_tiny_iteration_shapes_and_finiteness():
+    seqs = wl.tiny_iteration()
+
+    class S:
+        def __init__(self, it):
+            self.q_bits = it.stream.q[it.pos0:it.kv_len]
+            self.k_bits = it.stream.k[:it.kv_len]
+            self.v_bits = it.stream.v[:it.kv_len]
+    outs = oa.mixed_iteration([S(it) for it in seqs], 1.0 / np.sqrt(128))
+    assert [o.shape[0] for o in outs] == [128, 1, 1, 1, 1]
+    assert all(np.all(np.isfinite(o)) for o in outs)
+
+
+def test_rejects_bad_shapes():
+    with pytest.raises(ValueError):
+        oa.attention_sequence(np.zeros((2, 3, 8)), np.zeros((4, 2, 8)), np.zeros((4, 2, 8)), 1.0)
+    with pytest.raises(ValueError):
+        oa.attention_sequence(np.zeros((5, 2, 8)), np.zeros((4, 2, 8)), np.zeros((4, 2, 8)), 1.0)
