@@ -1,0 +1,240 @@
+/*
+ * dlfp.h -- C ABI of the mixed-iteration hot path of Decode-Latency Feedback
+ * Prefill (DLFP) on AMD Instinct MI355X (gfx950).
+ *
+ * One mixed continuous-batching iteration (Eq. 1, Sec. 2.1) serves the set
+ * D_t of decoding requests -- one new query token each -- together with p_t
+ * prompt tokens admitted for chunked prefill, which attend causally to their
+ * prompt's already-cached prefix plus the chunk itself (Sec. 2.1).  Keys and
+ * values live in a paged cache addressed through per-sequence block tables
+ * (PagedAttention, Sec. 2.1).  The iteration is:
+ *
+ *   dlfp_build_varlen_meta   host: packed-batch metadata and the work list
+ *   dlfp_kv_append           device: write this iteration's K/V into pages
+ *   dlfp_attention_mixed     device: ONE launch of attention for all rows
+ *   dlfp_controller_step     host: Eq. 2 on the completion-timed latency
+ *
+ * The iteration latency that feeds the controller is the completion time of
+ * the device work measured with HIP events (dlfp_timer_*), not the interval
+ * between scheduler calls -- the proxy the paper identifies as the reason its
+ * prototype failed to generalise (Sec. 3.2, Sec. 6.4, Sec. 11).
+ *
+ * Conventions for every call:
+ *  - Return value: DLFP_OK (0) or a negative dlfp_status.  No call throws,
+ *    aborts, prints, or synchronises a stream.  Validation happens before any
+ *    launch; on error nothing is launched and no output is written.
+ *  - Ownership: the caller owns every buffer (device and host).  The library
+ *    allocates no device memory and keeps no pointer after returning.
+ *  - Device calls are stream-ordered and asynchronous; a device-side fault
+ *    surfaces at the caller's next synchronisation.  A failed launch is
+ *    reported as DLFP_EHIP.
+ *  - Supported shapes: head_dim 128, page 16 tokens, Hq = g * Hkv with
+ *    g in {1, 2, 4, 8}; anything else is DLFP_EUNSUPPORTED.
+ *
+ * Device memory layouts (bf16 = IEEE bfloat16 stored as 16-bit words):
+ *  - q           [num_tokens][Hq][128]        packed in cu_q order
+ *  - k_new,v_new [num_tokens][Hkv][128]       this iteration's keys/values
+ *  - k_cache     [num_blocks][Hkv][16][128]   key page: 16 token rows
+ *  - v_cache     [num_blocks][Hkv][128][16]   value page: stored transposed,
+ *                                             one 32-byte row per dimension
+ *  - block_table [num_seqs][max_blocks] int32 physical block of each page
+ *  - out         [num_tokens][Hq][128]        bf16 or fp32
+ *  Token j of sequence s lives in block block_table[s][j / 16], slot j % 16;
+ *  its flat slot index is block * 16 + j % 16.
+ */
+#ifndef DLFP_H
+#define DLFP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DLFP_HEAD_DIM 128
+#define DLFP_PAGE_SIZE 16
+/* Query rows (tokens x grouped query heads) held by one prefill unit. */
+#define DLFP_TILE_ROWS 128
+/* int32 fields per work unit (see dlfp_build_varlen_meta). */
+#define DLFP_WORK_INTS 16
+/* Workspace layout: a 256-byte header (word 0 = error flag), then a fixed
+ * region of DLFP_MAX_GROUPS int32 split counters, then partial results from
+ * byte DLFP_WORKSPACE_PARTIALS on.  The counter region has the same size for
+ * every launch, so one workspace can serve iterations of any shape. */
+#define DLFP_WORKSPACE_HEADER 256
+#define DLFP_MAX_GROUPS 65536
+#define DLFP_WORKSPACE_PARTIALS (DLFP_WORKSPACE_HEADER + 4 * DLFP_MAX_GROUPS)
+
+typedef enum {
+  DLFP_OK = 0,
+  DLFP_EINVAL = -1,        /* malformed argument (null pointer, negative size, bad value) */
+  DLFP_ERANGE = -2,        /* index out of range (block id, sequence length vs table) */
+  DLFP_ENOSPC = -3,        /* caller-provided capacity or workspace too small */
+  DLFP_EHIP = -4,          /* a HIP runtime call or kernel launch failed */
+  DLFP_EUNSUPPORTED = -5   /* shape outside the supported set */
+} dlfp_status;
+
+/* Attention shape of one layer. */
+typedef struct {
+  int32_t num_q_heads;   /* Hq */
+  int32_t num_kv_heads;  /* Hkv; Hq / Hkv = g query heads share one KV head */
+  int32_t head_dim;      /* must be 128 */
+  int32_t page_size;     /* must be 16 */
+} dlfp_dims;
+
+/* How the attention launch splits key ranges (split-K).  Zero fields pick
+ * the built-in policy, which sizes splits so the launch has about
+ * target_units units of work. */
+typedef struct {
+  int32_t decode_split_tokens;   /* keys per decode unit; 0 = auto, else a multiple of 16 */
+  int32_t prefill_split_tokens;  /* keys per prefill unit; 0 = auto, else a multiple of 64 */
+  int32_t target_units;          /* auto policy target; 0 = 4096 */
+} dlfp_tuning;
+
+/* Host-side metadata of one packed batch.  The caller provides the arrays and
+ * their capacities; dlfp_build_varlen_meta fills arrays and counts. */
+typedef struct {
+  int32_t* cu_q;          /* [cap_seqs + 1] exclusive prefix sum of q_len */
+  int32_t* q_pos0;        /* [cap_seqs] absolute position of each sequence's first new token */
+  int32_t* slot_mapping;  /* [cap_tokens] flat pool slot of every new token, packed order */
+  int32_t* work;          /* [cap_work][DLFP_WORK_INTS] work units, see below */
+  int32_t cap_seqs, cap_tokens, cap_work;
+  /* filled on success */
+  int32_t num_seqs;
+  int32_t num_tokens;         /* sum of q_len */
+  int32_t num_units;          /* work units */
+  int32_t num_prefill_units;  /* the first num_prefill_units units are prefill tiles */
+  int32_t num_groups;         /* split groups (units sharing output rows) */
+  int32_t decode_split_tokens, prefill_split_tokens;  /* splits actually used */
+  int64_t workspace_bytes;    /* device workspace the attention launch needs */
+} dlfp_meta;
+
+/* Work unit fields (int32 index into one DLFP_WORK_INTS record). */
+enum {
+  DLFP_W_SEQ = 0,      /* sequence */
+  DLFP_W_KVHEAD = 1,   /* KV head; the unit serves its g query heads */
+  DLFP_W_QTOK0 = 2,    /* first new token of the sequence the unit serves (0-based) */
+  DLFP_W_QNTOK = 3,    /* number of new tokens it serves (1 for decode) */
+  DLFP_W_KVBEGIN = 4,  /* first key (multiple of 16) */
+  DLFP_W_KVEND = 5,    /* one past the last key */
+  DLFP_W_GROUP = 6,    /* split group, -1 when the unit alone covers its rows */
+  DLFP_W_SPLIT = 7,    /* index of this split within the group */
+  DLFP_W_NSPLITS = 8,  /* splits in the group */
+  DLFP_W_WSOFF = 9,    /* float offset of this unit's partial result in the workspace */
+  DLFP_W_WSGROUP = 10, /* float offset of the group's split 0 partial */
+  DLFP_W_KIND = 11     /* DLFP_KIND_PREFILL or DLFP_KIND_DECODE */
+};
+enum { DLFP_KIND_PREFILL = 0, DLFP_KIND_DECODE = 1 };
+
+/* Build the metadata of one mixed iteration (Eq. 1's D_t and p_t, Sec. 2.1).
+ *
+ * num_seqs sequences, each with q_len[s] >= 1 new tokens (1 for a decoder,
+ * the chunk size for a prefill slice) and kv_len[s] >= q_len[s] total keys
+ * including the new ones.  block_table is the HOST copy [num_seqs][max_blocks];
+ * every page a sequence uses must hold a block id in [0, num_blocks).
+ *
+ * Output (host arrays in *meta):
+ *   cu_q[s]   = sum_{r<s} q_len[r];   q_pos0[s] = kv_len[s] - q_len[s]
+ *   slot_mapping[cu_q[s] + i] = block_table[s][p / 16] * 16 + p % 16, p = q_pos0[s] + i
+ *   work: prefill units (sequences with q_len > 1) first, one per
+ *   (sequence, KV head, tile of DLFP_TILE_ROWS / g tokens, key split); then
+ *   decode units (q_len == 1), one per (sequence, KV head, key split).
+ *   Splits of the same rows form a group whose partial results the attention
+ *   launch combines in split order.
+ * Errors: DLFP_EINVAL (null pointers, q_len < 1, kv_len < q_len, bad tuning),
+ * DLFP_ERANGE (a used page's block id outside [0, num_blocks) or beyond
+ * max_blocks, or more than DLFP_MAX_GROUPS split groups), DLFP_ENOSPC (a capacity in *meta too small; the required counts
+ * are still written to num_seqs / num_tokens / num_units), DLFP_EUNSUPPORTED. */
+int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int32_t num_seqs,
+                           const int32_t* q_len, const int32_t* kv_len,
+                           const int32_t* block_table, int32_t max_blocks, int32_t num_blocks,
+                           dlfp_meta* meta);
+
+/* Write num_tokens new keys and values into their pages (PagedAttention cache
+ * write, Sec. 2.1 and Sec. 3.2).  k_new/v_new: device bf16 [num_tokens][Hkv][128];
+ * slot_mapping: device int32 [num_tokens] flat slots; caches as laid out above.
+ * Slots outside [0, num_blocks * 16) are skipped (never written).  Bit copy. */
+int dlfp_kv_append(const dlfp_dims* dims, int32_t num_tokens, const void* k_new,
+                   const void* v_new, const int32_t* slot_mapping, void* k_cache, void* v_cache,
+                   int32_t num_blocks, hipStream_t stream);
+
+/* One launch of masked softmax attention for every new token of the batch
+ * (the decode share and the prefill share of Eq. 1, Sec. 2.1).  For query
+ * row i of sequence s at position p = q_pos0[s] + i and query head h, with
+ * KV head h / g:  out = softmax_j(scale * q.k_j) v_j over keys j <= p.
+ *
+ * meta: the host metadata from dlfp_build_varlen_meta (only its counts are
+ * read).  d_cu_q, d_kv_len, d_q_pos0, d_work, d_block_table: device copies of
+ * meta->cu_q, the kv_len given to the builder, meta->q_pos0, meta->work and
+ * the block table.  q, k_cache, v_cache: device bf16.  out: device,
+ * out_dtype 0 = bf16, 1 = fp32.  workspace: device scratch of at least
+ * meta->workspace_bytes whose header and counter region (the first
+ * DLFP_WORKSPACE_PARTIALS bytes) were zeroed once by dlfp_workspace_init;
+ * every launch leaves the counters zero again.
+ * Launches sharing one workspace must be stream-ordered.
+ * Errors: DLFP_EINVAL, DLFP_ENOSPC (workspace too small), DLFP_EUNSUPPORTED,
+ * DLFP_EHIP.  A block id outside [0, num_blocks) met on the device is not
+ * read; the launch raises the workspace error word instead (dlfp_workspace_error). */
+int dlfp_attention_mixed(const dlfp_dims* dims, const dlfp_meta* meta, const int32_t* d_cu_q,
+                         const int32_t* d_kv_len, const int32_t* d_q_pos0, const int32_t* d_work,
+                         const int32_t* d_block_table, int32_t max_blocks, int32_t num_blocks,
+                         const void* q, const void* k_cache, const void* v_cache, float scale,
+                         void* out, int32_t out_dtype, void* workspace, size_t workspace_bytes,
+                         hipStream_t stream);
+
+/* Zero the workspace header and the whole counter region (the first
+ * DLFP_WORKSPACE_PARTIALS bytes) with a stream-ordered fill kernel.  Needed
+ * once per workspace allocation.  DLFP_ENOSPC if workspace_bytes is smaller. */
+int dlfp_workspace_init(void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Copy the workspace error word to *host_error after synchronising the stream:
+ * 0 = no error, 1 = a block id outside the pool was met. */
+int dlfp_workspace_error(const void* workspace, int32_t* host_error, hipStream_t stream);
+
+/* Proportional prefill-cap controller, Eq. 2 (Sec. 3.1):
+ *   cap <- clamp(quantum * floor(cap * target / observed / quantum), c_min, c_max)
+ * applied after each guarded cycle (at least one decoder and a prefill shared
+ * it).  When the next cycle has no decoder the cap resets to c_initial and
+ * prefill is uncapped (Sec. 3.1, Sec. 3.2).  Caller-owned plain struct. */
+typedef struct {
+  double target_ms;
+  int32_t c_initial, c_min, c_max, quantum;
+  int32_t cap;  /* current cap c_t */
+} dlfp_controller;
+
+/* Requires 0 < c_min <= c_initial <= c_max, quantum > 0, target_ms finite > 0. */
+int dlfp_controller_init(dlfp_controller* ctrl, double target_ms, int32_t c_initial,
+                         int32_t c_min, int32_t c_max, int32_t quantum);
+
+/* After a cycle has COMPLETED: if last_was_guarded, update the cap from
+ * observed_ms (the cycle's device completion time); then, if
+ * num_decoding_next == 0, reset.  *next_cap receives the cap for the next
+ * cycle's prefill, or -1 (uncapped) when no decoder is active.
+ * DLFP_EINVAL if observed_ms is not finite and positive while
+ * last_was_guarded (state unchanged). */
+int dlfp_controller_step(dlfp_controller* ctrl, int32_t num_decoding_next,
+                         int32_t last_was_guarded, double observed_ms, int32_t* next_cap);
+
+/* Completion timer: a pair of HIP events around an iteration's device work.
+ * The handle owns two events (no device memory). */
+typedef struct dlfp_timer_s* dlfp_timer;
+int dlfp_timer_create(dlfp_timer* timer);
+int dlfp_timer_destroy(dlfp_timer timer);
+int dlfp_timer_start(dlfp_timer timer, hipStream_t stream);
+int dlfp_timer_stop(dlfp_timer timer, hipStream_t stream);
+/* Block until the stop event has completed; elapsed device time in ms. */
+int dlfp_timer_elapsed_ms(dlfp_timer timer, double* ms);
+
+const char* dlfp_status_string(int status);
+
+/* Library version, e.g. 100 for 0.1.0. */
+int dlfp_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DLFP_H */

@@ -24,6 +24,8 @@ import numpy as np
 PAGE = 16
 HEAD_DIM = 128
 TILE_ROWS = 128          # query rows (tokens x grouped heads) one prefill unit holds
+WS_HEADER = 256          # workspace bytes before the split counters
+WS_MAX_GROUPS = 65536    # fixed counter region: one int32 per possible group
 
 # Work-item field indices (16 int32 per unit).
 W_SEQ, W_KVHEAD, W_QTOK0, W_QNTOK, W_KVBEGIN, W_KVEND = 0, 1, 2, 3, 4, 5
@@ -71,7 +73,10 @@ def check_work_list(work: np.ndarray, num_prefill: int, q_len: Sequence[int],
     work = np.asarray(work, dtype=np.int64).reshape(-1, WORK_INTS)
     counts = {}
     groups: Dict[int, List[np.ndarray]] = {}
-    partial_base = ((num_groups * 4 + 255) // 256 * 256) // 4
+    # workspace: header, the fixed counter region, then partial slots
+    if num_groups > WS_MAX_GROUPS:
+        fail("more groups than counters")
+    partial_base = (WS_HEADER + 4 * WS_MAX_GROUPS) // 4
     slots = []
     for u, it in enumerate(work):
         s, kh, t0, nt, kb, ke = (int(x) for x in it[:6])
@@ -147,6 +152,6 @@ def check_work_list(work: np.ndarray, num_prefill: int, q_len: Sequence[int],
             fail("partial slots overlap")
     if slots and slots[-1][1] * 4 > workspace_bytes:
         fail("partial slots exceed the workspace")
-    if num_groups * 4 > workspace_bytes and num_groups:
-        fail("counters exceed the workspace")
+    if WS_HEADER + 4 * WS_MAX_GROUPS > workspace_bytes:
+        fail("header and counters exceed the workspace")
     return {"units": len(work), "groups": len(groups)}

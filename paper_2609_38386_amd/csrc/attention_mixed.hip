@@ -1,0 +1,731 @@
+// Single-launch paged attention for one mixed continuous-batching iteration:
+// the decode share (one query token per decoding request) and the prefill
+// share (a chunk of prompt tokens, causal over the prompt's cached prefix plus
+// the chunk) of Eq. 1, Sec. 2.1, served by one grid.
+//
+// Grid: the work list's prefill units first, one 256-thread workgroup each,
+// then decode units, four per workgroup (one per wavefront).
+//
+// Prefill unit = (sequence, KV head, tile of 128 query rows, key split).
+// Rows are the tile's tokens x the g query heads sharing the KV head, so each
+// K/V tile staged in LDS serves all g heads (grouped-query sharing in LDS).
+// Each wavefront owns 32 rows and computes, per 64-key tile,
+//   S^T = K Q^T        (v_mfma_f32_32x32x16_bf16, fp32 accumulation)
+//   online softmax     (exp2 domain; each lane owns one row, so row max and
+//                       sum need only one exchange with lane ^ 32)
+//   O^T += V^T P^T     (P rounded to bf16; V pages are stored transposed, so
+//                       the operand is read straight from LDS)
+// Working with S^T and O^T keeps every row statistic lane-local, and the
+// accumulator layout of S^T is already the B-operand layout of the PV
+// product, so P never leaves registers.  K/V tiles are double-buffered in LDS
+// (one barrier per tile), with XOR swizzles that keep the 16 lanes of each
+// LDS access phase on distinct banks.
+//
+// Decode unit = (sequence, KV head, key split), one wavefront.  Memory-bound:
+// each 16-token page of K and V (8 KiB) is fetched with fully coalesced
+// 16-byte loads one page ahead, staged in the wave's LDS slice, and consumed by
+// VALU bf16 dot products (v_dot2 with fp32 accumulation).  Eight lanes share a
+// key (16 dims each) and sum their partial dot products with DPP; the
+// per-head row max uses DPP and wavefront shuffles; probabilities are handed
+// to the PV lanes through LDS, and each lane owns two output dims.
+//
+// Split-K: a unit whose rows are split over several key ranges writes
+// (unnormalised O, running max, running sum) to its workspace slot, releases,
+// and bumps its group's counter; the last arriver acquires and merges all
+// splits in split-index order (deterministic), writes the output and resets
+// the counter to zero for the next launch.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "dlfp.h"
+#include "dlfp_internal.h"
+
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+
+constexpr int D = DLFP_HEAD_DIM;
+constexpr int PAGE = DLFP_PAGE_SIZE;
+constexpr int PAGE_ELEMS = PAGE * D;          // bf16 elements per (block, head) page
+constexpr int KV_TILE = 64;                   // keys per prefill tile (4 pages)
+constexpr int THREADS = 256;
+constexpr int STAGE_BYTES = 2 * KV_TILE * D * 2;   // K tile + V^T tile
+constexpr int LDS_BYTES = 2 * STAGE_BYTES;         // double buffered: 64 KiB
+constexpr int DEC_WAVE_LDS = 2 * PAGE_ELEMS * 2 + 16 * 16 * 2;  // K page, V page, p buffer
+constexpr float NEG_BIG = -1.0e30f;
+constexpr float LOG2E = 1.4426950408889634f;
+
+static_assert(4 * DEC_WAVE_LDS <= LDS_BYTES, "decode slices must fit the shared buffer");
+
+struct Args {
+  const int32_t* cu_q;
+  const int32_t* kv_len;
+  const int32_t* q_pos0;
+  const int32_t* work;
+  const int32_t* block_table;
+  const uint16_t* q;
+  const uint16_t* kc;
+  const uint16_t* vc;
+  void* out;
+  float* ws;
+  int32_t max_blocks;
+  int32_t num_blocks;
+  int32_t hq;
+  int32_t hkv;
+  int32_t num_units;
+  int32_t num_prefill;
+  int32_t out_f32;
+  float scale_log2;  // softmax scale * log2(e)
+};
+
+__device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a),
+                                         __builtin_bit_cast(bf16x2_t, b), c, false);
+}
+
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
+  bf16x2_t v;
+  v[0] = (__bf16)lo;
+  v[1] = (__bf16)hi;
+  return __builtin_bit_cast(uint32_t, v);
+}
+
+__device__ __forceinline__ float fexp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+template <int CTRL>
+__device__ __forceinline__ float dpp(float x) {
+  return __builtin_bit_cast(
+      float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xF, 0xF, false));
+}
+constexpr int DPP_XOR1 = 0xB1;         // quad_perm [1,0,3,2]
+constexpr int DPP_XOR2 = 0x4E;         // quad_perm [2,3,0,1]
+constexpr int DPP_HALF_MIRROR = 0x141; // lane i <-> 7 - i within 8 lanes
+constexpr int DPP_ROR8 = 0x128;        // rotate a 16-lane row by 8
+
+__device__ __forceinline__ float shfl_xor(float x, int m) { return __shfl_xor(x, m); }
+
+__device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+// Lanes of one wavefront hand data to each other through LDS.  The hardware
+// runs a wave's LDS operations in order; this keeps the compiler from moving a
+// lane's LDS accesses across the hand-off (it reasons per lane, so a store to
+// an address the lane itself never reads would otherwise be free to move).
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+__device__ __forceinline__ void raise_error(float* ws) {
+  __hip_atomic_store(reinterpret_cast<int*>(ws), 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ int* group_counter(float* ws, int grp) {
+  return reinterpret_cast<int*>(reinterpret_cast<char*>(ws) + DLFP_WORKSPACE_HEADER) + grp;
+}
+
+// Workgroups are dealt round-robin over the 8 XCDs; map them so that each XCD
+// gets a contiguous range of prefill units (same KV head -> same L2).
+__device__ __forceinline__ int xcd_remap(int b, int n) {
+  const int x = b & 7, i = b >> 3;
+  const int per = n >> 3, rem = n & 7;
+  return x * per + min(x, rem) + i;
+}
+
+// Store 4 consecutive output values of one row.
+__device__ __forceinline__ void store4(const Args& a, int64_t elem, float v0, float v1, float v2,
+                                       float v3) {
+  if (a.out_f32) {
+    f32x4_t v = {v0, v1, v2, v3};
+    *reinterpret_cast<f32x4_t*>(static_cast<float*>(a.out) + elem) = v;
+  } else {
+    u32x2_t v = {pack_bf16(v0, v1), pack_bf16(v2, v3)};
+    *reinterpret_cast<u32x2_t*>(static_cast<uint16_t*>(a.out) + elem) = v;
+  }
+}
+
+__device__ __forceinline__ void store2(const Args& a, int64_t elem, float v0, float v1) {
+  if (a.out_f32) {
+    f32x2_t v = {v0, v1};
+    *reinterpret_cast<f32x2_t*>(static_cast<float*>(a.out) + elem) = v;
+  } else {
+    *reinterpret_cast<uint32_t*>(static_cast<uint16_t*>(a.out) + elem) = pack_bf16(v0, v1);
+  }
+}
+
+// Keep the lanes of a 16-bit-element vector whose key index is < limit; zero the rest.
+__device__ __forceinline__ u32x4_t mask_keys(u32x4_t v, int key0, int limit) {
+  const int n = limit - key0;  // elements e < n survive
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    const uint32_t lo = (2 * w < n) ? 0x0000FFFFu : 0u;
+    const uint32_t hi = (2 * w + 1 < n) ? 0xFFFF0000u : 0u;
+    v[w] &= (lo | hi);
+  }
+  return v;
+}
+
+// ---------------------------------------------------------------- prefill
+
+// One 64-key stage: 4 pages of K and 4 pages of V^T; thread t moves 16-byte
+// chunk t of each page (a page is 256 chunks).
+struct Stage {
+  u32x4_t c[8];
+};
+
+__device__ __forceinline__ void load_stage(Stage& st, const Args& a, const int32_t* bt, int kh,
+                                           int k0, int ke, int tid) {
+#pragma unroll
+  for (int pg = 0; pg < 4; ++pg) {
+    const int key0 = k0 + pg * PAGE;
+    u32x4_t kv = {0, 0, 0, 0}, vv = {0, 0, 0, 0};
+    if (key0 < ke) {
+      const int blk = bt[key0 / PAGE];
+      if ((unsigned)blk < (unsigned)a.num_blocks) {
+        const int64_t base = ((int64_t)blk * a.hkv + kh) * PAGE_ELEMS + tid * 8;
+        kv = *reinterpret_cast<const u32x4_t*>(a.kc + base);
+        vv = *reinterpret_cast<const u32x4_t*>(a.vc + base);
+      } else if (tid == 0) {
+        raise_error(a.ws);
+      }
+    }
+    st.c[pg] = kv;
+    st.c[4 + pg] = vv;
+  }
+}
+
+// K tile in LDS: row R (key) is 256 bytes; 16-byte chunk x sits at x ^ (R & 15).
+// V^T tile: page pg at 16 KiB + pg * 4 KiB, dim d row of 32 bytes; 8-byte slot
+// s (keys 4s..4s+3) sits at s ^ ((d >> 2) & 3).
+__device__ __forceinline__ void store_stage(const Stage& st, char* buf, int tid, int k0, int ke) {
+#pragma unroll
+  for (int pg = 0; pg < 4; ++pg) {
+    const int row = tid >> 4, x = tid & 15;
+    const int R = pg * PAGE + row;
+    *reinterpret_cast<u32x4_t*>(buf + R * 256 + ((x ^ (R & 15)) << 4)) = st.c[pg];
+  }
+#pragma unroll
+  for (int pg = 0; pg < 4; ++pg) {
+    const int d = tid >> 1, half = tid & 1;
+    u32x4_t v = st.c[4 + pg];
+    const int key0 = k0 + pg * PAGE + 8 * half;
+    if (key0 + 8 > ke) v = mask_keys(v, key0, ke);
+    const int f = (d >> 2) & 3;
+    char* rowp = buf + KV_TILE * D * 2 + pg * PAGE_ELEMS * 2 + d * 32;
+    u32x2_t lo = {v[0], v[1]}, hi = {v[2], v[3]};
+    *reinterpret_cast<u32x2_t*>(rowp + (((2 * half) ^ f) << 3)) = lo;
+    *reinterpret_cast<u32x2_t*>(rowp + (((2 * half + 1) ^ f) << 3)) = hi;
+  }
+}
+
+template <int G>
+__device__ void prefill_unit(const Args& a, const int32_t* it, char* smem, int* flag) {
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int col = lane & 31, hi = lane >> 5;
+  const int s = it[DLFP_W_SEQ], kh = it[DLFP_W_KVHEAD];
+  const int t0 = it[DLFP_W_QTOK0], nt = it[DLFP_W_QNTOK];
+  const int kb = it[DLFP_W_KVBEGIN], ke = it[DLFP_W_KVEND];
+  const int nsplits = it[DLFP_W_NSPLITS];
+  const int q0 = a.cu_q[s], pos0 = a.q_pos0[s];
+  const int32_t* bt = a.block_table + (int64_t)s * a.max_blocks;
+
+  const int r = wave * 32 + col;       // this lane's row within the tile
+  const int tr = r / G, hh = r % G;    // token within the unit, head within the group
+  const bool row_ok = tr < nt;
+  const int lim = row_ok ? min(pos0 + t0 + tr + 1, ke) : 0;  // keys < lim are visible
+  const int wave_tok0 = (wave * 32) / G;
+  const bool wave_active = wave_tok0 < nt;
+  const int wave_lim_min = min(pos0 + t0 + wave_tok0 + 1, ke);
+
+  // Q^T as the B operand: lane holds dims [16kk + 8hi, +8) of its row.
+  bf16x8_t qf[8];
+  {
+    const int64_t qrow = ((int64_t)(q0 + t0 + (row_ok ? tr : 0)) * a.hq + kh * G + hh) * D;
+#pragma unroll
+    for (int kk = 0; kk < 8; ++kk) {
+      u32x4_t v = {0, 0, 0, 0};
+      if (row_ok) v = *reinterpret_cast<const u32x4_t*>(a.q + qrow + 16 * kk + 8 * hi);
+      qf[kk] = __builtin_bit_cast(bf16x8_t, v);
+    }
+  }
+
+  float m_run = NEG_BIG, l_run = 0.f;
+  f32x16_t o[4];
+#pragma unroll
+  for (int mb = 0; mb < 4; ++mb) o[mb] = f32x16_t{};
+
+  const int ntiles = (ke - kb + KV_TILE - 1) / KV_TILE;
+  Stage st;
+  load_stage(st, a, bt, kh, kb, ke, tid);
+  store_stage(st, smem, tid, kb, ke);
+  __syncthreads();
+
+  for (int ti = 0; ti < ntiles; ++ti) {
+    const int k0 = kb + ti * KV_TILE;
+    const bool more = ti + 1 < ntiles;
+    if (more) load_stage(st, a, bt, kh, k0 + KV_TILE, ke, tid);
+    const char* buf = smem + (ti & 1) * STAGE_BYTES;
+
+    if (wave_active) {
+      // S^T = K Q^T for keys [k0, k0 + 64): two 32-key blocks.
+      f32x16_t sacc[2];
+#pragma unroll
+      for (int kb2 = 0; kb2 < 2; ++kb2) {
+        sacc[kb2] = f32x16_t{};
+        const int R = kb2 * 32 + col;
+#pragma unroll
+        for (int kk = 0; kk < 8; ++kk) {
+          const int x = 2 * kk + hi;
+          const bf16x8_t af =
+              *reinterpret_cast<const bf16x8_t*>(buf + R * 256 + ((x ^ (R & 15)) << 4));
+          sacc[kb2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, qf[kk], sacc[kb2], 0, 0, 0);
+        }
+      }
+      // Scale, mask, running max.  sacc[kb2][rr] holds key
+      // 32 kb2 + 8 (rr / 4) + 4 hi + rr % 4 of this lane's row.
+      const bool need_mask = k0 + KV_TILE > wave_lim_min;
+      float mx = NEG_BIG;
+#pragma unroll
+      for (int kb2 = 0; kb2 < 2; ++kb2)
+#pragma unroll
+        for (int rr = 0; rr < 16; ++rr) {
+          float x = sacc[kb2][rr] * a.scale_log2;
+          if (need_mask) {
+            const int key = k0 + kb2 * 32 + 8 * (rr >> 2) + 4 * hi + (rr & 3);
+            x = key < lim ? x : -__builtin_inff();
+          }
+          sacc[kb2][rr] = x;
+          mx = fmaxf(mx, x);
+        }
+      mx = fmaxf(mx, shfl_xor(mx, 32));
+      const float m_new = fmaxf(m_run, mx);
+      const float alpha = fexp2(m_run - m_new);
+      m_run = m_new;
+      float psum = 0.f;
+      bf16x8_t pf[4];
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {
+        u32x4_t pk;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          const float p0 = fexp2(sacc[kk >> 1][8 * (kk & 1) + 2 * w] - m_new);
+          const float p1 = fexp2(sacc[kk >> 1][8 * (kk & 1) + 2 * w + 1] - m_new);
+          psum += p0 + p1;
+          pk[w] = pack_bf16(p0, p1);
+        }
+        pf[kk] = __builtin_bit_cast(bf16x8_t, pk);
+      }
+      l_run = l_run * alpha + psum;
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb) o[mb] *= alpha;
+      // O^T += V^T P^T, one 16-key page per k-step.
+      const char* vbuf = buf + KV_TILE * D * 2;
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {
+        const char* vp = vbuf + kk * PAGE_ELEMS * 2;
+#pragma unroll
+        for (int mb = 0; mb < 4; ++mb) {
+          const int d = mb * 32 + col;
+          const int f = (d >> 2) & 3;
+          const u32x2_t lo = *reinterpret_cast<const u32x2_t*>(vp + d * 32 + ((hi ^ f) << 3));
+          const u32x2_t hv =
+              *reinterpret_cast<const u32x2_t*>(vp + d * 32 + (((2 + hi) ^ f) << 3));
+          const u32x4_t av = {lo[0], lo[1], hv[0], hv[1]};
+          o[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, av),
+                                                          pf[kk], o[mb], 0, 0, 0);
+        }
+      }
+    }
+    if (more) store_stage(st, smem + ((ti + 1) & 1) * STAGE_BYTES, tid, k0 + KV_TILE, ke);
+    __syncthreads();
+  }
+
+  l_run += shfl_xor(l_run, 32);
+  const int rows = nt * G;
+  // o[mb][rr] = O[row][32 mb + 8 (rr / 4) + 4 hi + rr % 4]
+  if (nsplits == 1) {
+    if (row_ok) {
+      const float inv = 1.f / l_run;
+      const int64_t orow = ((int64_t)(q0 + t0 + tr) * a.hq + kh * G + hh) * D;
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+        for (int g4 = 0; g4 < 4; ++g4)
+          store4(a, orow + mb * 32 + 8 * g4 + 4 * hi, o[mb][4 * g4] * inv,
+                 o[mb][4 * g4 + 1] * inv, o[mb][4 * g4 + 2] * inv, o[mb][4 * g4 + 3] * inv);
+    }
+    return;
+  }
+
+  // Partial result: O[rows][128], then m[rows], then l[rows].
+  float* slot = a.ws + it[DLFP_W_WSOFF];
+  if (row_ok) {
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4) {
+        f32x4_t v = {o[mb][4 * g4], o[mb][4 * g4 + 1], o[mb][4 * g4 + 2], o[mb][4 * g4 + 3]};
+        *reinterpret_cast<f32x4_t*>(slot + r * D + mb * 32 + 8 * g4 + 4 * hi) = v;
+      }
+    if (hi == 0) {
+      slot[rows * D + r] = m_run;
+      slot[rows * D + rows + r] = l_run;
+    }
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  __syncthreads();
+  const int grp = it[DLFP_W_GROUP];
+  if (tid == 0) {
+    const int old = __hip_atomic_fetch_add(group_counter(a.ws, grp), 1, __ATOMIC_ACQ_REL,
+                                           __HIP_MEMORY_SCOPE_AGENT);
+    *flag = old == nsplits - 1;
+  }
+  __syncthreads();
+  if (!*flag) return;
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+
+  // Last arriver: merge every split of the group in split order.
+  const float* g0 = a.ws + it[DLFP_W_WSGROUP];
+  const int slot_floats = rows * (D + 2);
+  for (int f = tid; f < rows * (D / 4); f += THREADS) {
+    const int row = f / (D / 4), c4 = f % (D / 4);
+    float mmax = NEG_BIG;
+    for (int j = 0; j < nsplits; ++j) mmax = fmaxf(mmax, g0[j * slot_floats + rows * D + row]);
+    float lsum = 0.f;
+    f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < nsplits; ++j) {
+      const float* sj = g0 + j * slot_floats;
+      const float w = fexp2(sj[rows * D + row] - mmax);
+      lsum += w * sj[rows * D + rows + row];
+      acc += w * *reinterpret_cast<const f32x4_t*>(sj + row * D + 4 * c4);
+    }
+    const float inv = 1.f / lsum;
+    const int trow = row / G, hrow = row % G;
+    const int64_t orow = ((int64_t)(q0 + t0 + trow) * a.hq + kh * G + hrow) * D;
+    store4(a, orow + 4 * c4, acc[0] * inv, acc[1] * inv, acc[2] * inv, acc[3] * inv);
+  }
+  if (tid == 0)
+    __hip_atomic_store(group_counter(a.ws, grp), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// ---------------------------------------------------------------- decode
+
+// Wave-private LDS slice: K page (token rows, 16-byte chunk x of row R at
+// x ^ 8 (R & 1)), V^T page (64-byte dim-pair region r, 16-byte slot i at
+// (i + r / 4) & 3), then the probability buffer p[head][16 keys] in bf16.
+template <int G>
+__device__ void decode_unit(const Args& a, const int32_t* it, char* wl) {
+  const int lane = threadIdx.x & 63;
+  const int kg = lane >> 3, c = lane & 7;
+  const int s = uniform(it[DLFP_W_SEQ]), kh = uniform(it[DLFP_W_KVHEAD]);
+  const int kb = uniform(it[DLFP_W_KVBEGIN]), ke = uniform(it[DLFP_W_KVEND]);
+  const int nsplits = uniform(it[DLFP_W_NSPLITS]);
+  const int tok = uniform(a.cu_q[s]);
+  const int32_t* bt = a.block_table + (int64_t)s * a.max_blocks;
+  char* kl = wl;
+  char* vl = wl + PAGE_ELEMS * 2;
+  uint16_t* pbuf = reinterpret_cast<uint16_t*>(wl + 2 * PAGE_ELEMS * 2);
+
+  // Query of the g heads: lane holds dims [8c, 8c + 8) and [64 + 8c, 64 + 8c + 8).
+  u32x4_t qa[G], qb[G];
+  {
+    const uint16_t* qp = a.q + ((int64_t)tok * a.hq + kh * G) * D;
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      qa[h] = *reinterpret_cast<const u32x4_t*>(qp + h * D + 8 * c);
+      qb[h] = *reinterpret_cast<const u32x4_t*>(qp + h * D + 64 + 8 * c);
+    }
+  }
+  float m[G], l[G], o0[G], o1[G];
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    m[h] = NEG_BIG;
+    l[h] = 0.f;
+    o0[h] = 0.f;
+    o1[h] = 0.f;
+  }
+
+  const int p_begin = kb / PAGE, p_end = (ke + PAGE - 1) / PAGE;
+  u32x4_t fk[4], fv[4];
+  auto fetch = [&](int p) {
+    const int blk = bt[p];
+    if ((unsigned)blk < (unsigned)a.num_blocks) {
+      const int64_t base = ((int64_t)blk * a.hkv + kh) * PAGE_ELEMS;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        fk[j] = *reinterpret_cast<const u32x4_t*>(a.kc + base + (64 * j + lane) * 8);
+        fv[j] = *reinterpret_cast<const u32x4_t*>(a.vc + base + (64 * j + lane) * 8);
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        fk[j] = u32x4_t{0, 0, 0, 0};
+        fv[j] = u32x4_t{0, 0, 0, 0};
+      }
+      if (lane == 0) raise_error(a.ws);
+    }
+  };
+  fetch(p_begin);
+
+  for (int p = p_begin; p < p_end; ++p) {
+    // Stage the fetched page in LDS.
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int q = 64 * j + lane;
+      const int R = q >> 4, x = q & 15;
+      *reinterpret_cast<u32x4_t*>(kl + R * 256 + ((x ^ ((R & 1) << 3)) << 4)) = fk[j];
+      const int rg = q >> 2, si = q & 3;
+      u32x4_t v = fv[j];
+      const int key0 = p * PAGE + 8 * (si & 1);
+      if (key0 + 8 > ke) v = mask_keys(v, key0, ke);
+      *reinterpret_cast<u32x4_t*>(vl + rg * 64 + (((si + (rg >> 2)) & 3) << 4)) = v;
+    }
+    if (p + 1 < p_end) fetch(p + 1);
+    wave_sync();  // staged page visible to every lane
+
+    // Scores of keys 8 st + kg, reduced over the 8 lanes of each key.
+    float sc[2][G];
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
+      const int R = 8 * st + kg;
+      const u32x4_t k0v =
+          *reinterpret_cast<const u32x4_t*>(kl + R * 256 + ((c ^ ((R & 1) << 3)) << 4));
+      const u32x4_t k1v =
+          *reinterpret_cast<const u32x4_t*>(kl + R * 256 + (((c + 8) ^ ((R & 1) << 3)) << 4));
+      const bool valid = p * PAGE + R < ke;
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        float acc = 0.f;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) acc = dot2(qa[h][w], k0v[w], acc);
+#pragma unroll
+        for (int w = 0; w < 4; ++w) acc = dot2(qb[h][w], k1v[w], acc);
+        acc += dpp<DPP_XOR1>(acc);
+        acc += dpp<DPP_XOR2>(acc);
+        acc += dpp<DPP_HALF_MIRROR>(acc);
+        sc[st][h] = valid ? acc * a.scale_log2 : -__builtin_inff();
+      }
+    }
+    // Online softmax per head.
+    float alpha[G];
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      float mx = fmaxf(sc[0][h], sc[1][h]);
+      mx = fmaxf(mx, dpp<DPP_ROR8>(mx));
+      mx = fmaxf(mx, shfl_xor(mx, 16));
+      mx = fmaxf(mx, shfl_xor(mx, 32));
+      const float m_new = fmaxf(m[h], mx);
+      alpha[h] = fexp2(m[h] - m_new);
+      m[h] = m_new;
+      const float p0 = fexp2(sc[0][h] - m_new), p1 = fexp2(sc[1][h] - m_new);
+      l[h] = l[h] * alpha[h] + (c == 0 ? p0 + p1 : 0.f);
+      if (c == (h & 7)) {
+        pbuf[h * 16 + kg] = __builtin_bit_cast(uint16_t, (__bf16)p0);
+        pbuf[h * 16 + 8 + kg] = __builtin_bit_cast(uint16_t, (__bf16)p1);
+      }
+    }
+    wave_sync();  // probabilities visible to every lane
+    // O += P V: lane owns dims 2 lane and 2 lane + 1.
+    u32x4_t vr[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      vr[i] = *reinterpret_cast<const u32x4_t*>(vl + lane * 64 + (((i + (lane >> 2)) & 3) << 4));
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      const u32x4_t pp0 = *reinterpret_cast<const u32x4_t*>(pbuf + h * 16);
+      const u32x4_t pp1 = *reinterpret_cast<const u32x4_t*>(pbuf + h * 16 + 8);
+      float a0 = o0[h] * alpha[h], a1 = o1[h] * alpha[h];
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        a0 = dot2(pp0[w], vr[0][w], a0);
+        a1 = dot2(pp0[w], vr[2][w], a1);
+      }
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        a0 = dot2(pp1[w], vr[1][w], a0);
+        a1 = dot2(pp1[w], vr[3][w], a1);
+      }
+      o0[h] = a0;
+      o1[h] = a1;
+    }
+    wave_sync();  // every lane done reading before the next page overwrites LDS
+  }
+
+  // Row sums live on the c == 0 lanes; total them.
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    float x = l[h];
+    x += dpp<DPP_ROR8>(x);
+    x += shfl_xor(x, 16);
+    x += shfl_xor(x, 32);
+    l[h] = __builtin_bit_cast(float, uniform(__builtin_bit_cast(int, x)));
+  }
+
+  const int64_t obase = ((int64_t)tok * a.hq + kh * G) * D + 2 * lane;
+  if (nsplits == 1) {
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      const float inv = 1.f / l[h];
+      store2(a, obase + h * D, o0[h] * inv, o1[h] * inv);
+    }
+    return;
+  }
+
+  // Partial: O[G][128], m[G], l[G].
+  float* slot = a.ws + uniform(it[DLFP_W_WSOFF]);
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    f32x2_t v = {o0[h], o1[h]};
+    *reinterpret_cast<f32x2_t*>(slot + h * D + 2 * lane) = v;
+    if (lane == 0) {
+      slot[G * D + h] = m[h];
+      slot[G * D + G + h] = l[h];
+    }
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  const int grp = uniform(it[DLFP_W_GROUP]);
+  int old = 0;
+  if (lane == 0)
+    old = __hip_atomic_fetch_add(group_counter(a.ws, grp), 1, __ATOMIC_ACQ_REL,
+                                 __HIP_MEMORY_SCOPE_AGENT);
+  old = __shfl(old, 0);
+  if (old != nsplits - 1) return;
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+
+  const float* g0 = a.ws + uniform(it[DLFP_W_WSGROUP]);
+  const int slot_floats = G * (D + 2);
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    float mmax = NEG_BIG;
+    for (int j = 0; j < nsplits; ++j) mmax = fmaxf(mmax, g0[j * slot_floats + G * D + h]);
+    float lsum = 0.f, acc0 = 0.f, acc1 = 0.f;
+    for (int j = 0; j < nsplits; ++j) {
+      const float* sj = g0 + j * slot_floats;
+      const float w = fexp2(sj[G * D + h] - mmax);
+      lsum += w * sj[G * D + G + h];
+      const f32x2_t v = *reinterpret_cast<const f32x2_t*>(sj + h * D + 2 * lane);
+      acc0 += w * v[0];
+      acc1 += w * v[1];
+    }
+    const float inv = 1.f / lsum;
+    store2(a, obase + h * D, acc0 * inv, acc1 * inv);
+  }
+  if (lane == 0)
+    __hip_atomic_store(group_counter(a.ws, grp), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// ---------------------------------------------------------------- kernel
+
+template <int G>
+__global__ __launch_bounds__(THREADS, 2) void attention_mixed_kernel(Args a) {
+  __shared__ __attribute__((aligned(16))) char smem[LDS_BYTES];
+  __shared__ int flag;
+  const int b = blockIdx.x;
+  if (b < a.num_prefill) {
+    const int u = xcd_remap(b, a.num_prefill);
+    prefill_unit<G>(a, a.work + (int64_t)u * DLFP_WORK_INTS, smem, &flag);
+  } else {
+    const int wave = threadIdx.x >> 6;
+    const int u = a.num_prefill + (b - a.num_prefill) * 4 + wave;
+    if (u >= a.num_units) return;
+    decode_unit<G>(a, a.work + (int64_t)u * DLFP_WORK_INTS, smem + wave * DEC_WAVE_LDS);
+  }
+}
+
+__global__ void fill_zero_kernel(int* p, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0;
+}
+
+template <int G>
+hipError_t launch(const Args& a, int grid, hipStream_t stream) {
+  attention_mixed_kernel<G><<<grid, THREADS, 0, stream>>>(a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+extern "C" int dlfp_attention_mixed(const dlfp_dims* dims, const dlfp_meta* meta,
+                                    const int32_t* d_cu_q, const int32_t* d_kv_len,
+                                    const int32_t* d_q_pos0, const int32_t* d_work,
+                                    const int32_t* d_block_table, int32_t max_blocks,
+                                    int32_t num_blocks, const void* q, const void* k_cache,
+                                    const void* v_cache, float scale, void* out,
+                                    int32_t out_dtype, void* workspace, size_t workspace_bytes,
+                                    hipStream_t stream) {
+  int g = 0;
+  const int st = dlfp::check_dims(dims, &g);
+  if (st != DLFP_OK) return st;
+  if (!meta) return DLFP_EINVAL;
+  if (out_dtype != 0 && out_dtype != 1) return DLFP_EINVAL;
+  if (!(scale > 0.f) || !(scale < 3.0e38f)) return DLFP_EINVAL;
+  if (meta->num_units < 0 || meta->num_prefill_units < 0 ||
+      meta->num_prefill_units > meta->num_units || meta->num_groups < 0)
+    return DLFP_EINVAL;
+  if (meta->num_units == 0) return DLFP_OK;
+  if (!d_cu_q || !d_kv_len || !d_q_pos0 || !d_work || !d_block_table || !q || !k_cache ||
+      !v_cache || !out || !workspace)
+    return DLFP_EINVAL;
+  if (max_blocks <= 0 || num_blocks <= 0) return DLFP_EINVAL;
+  if ((int64_t)workspace_bytes < meta->workspace_bytes ||
+      workspace_bytes < (size_t)DLFP_WORKSPACE_PARTIALS)
+    return DLFP_ENOSPC;
+  if (meta->num_groups > DLFP_MAX_GROUPS) return DLFP_EINVAL;
+  Args a;
+  a.cu_q = d_cu_q;
+  a.kv_len = d_kv_len;
+  a.q_pos0 = d_q_pos0;
+  a.work = d_work;
+  a.block_table = d_block_table;
+  a.q = static_cast<const uint16_t*>(q);
+  a.kc = static_cast<const uint16_t*>(k_cache);
+  a.vc = static_cast<const uint16_t*>(v_cache);
+  a.out = out;
+  a.ws = static_cast<float*>(workspace);
+  a.max_blocks = max_blocks;
+  a.num_blocks = num_blocks;
+  a.hq = dims->num_q_heads;
+  a.hkv = dims->num_kv_heads;
+  a.num_units = meta->num_units;
+  a.num_prefill = meta->num_prefill_units;
+  a.out_f32 = out_dtype;
+  a.scale_log2 = scale * LOG2E;
+  const int decode_units = meta->num_units - meta->num_prefill_units;
+  const int grid = meta->num_prefill_units + (decode_units + 3) / 4;
+  (void)hipGetLastError();
+  hipError_t e;
+  switch (g) {
+    case 1: e = launch<1>(a, grid, stream); break;
+    case 2: e = launch<2>(a, grid, stream); break;
+    case 4: e = launch<4>(a, grid, stream); break;
+    default: e = launch<8>(a, grid, stream); break;
+  }
+  return e == hipSuccess ? DLFP_OK : DLFP_EHIP;
+}
+
+extern "C" int dlfp_workspace_init(void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (!workspace) return DLFP_EINVAL;
+  const int64_t bytes = DLFP_WORKSPACE_PARTIALS;
+  if ((int64_t)workspace_bytes < bytes) return DLFP_ENOSPC;
+  const int64_t n = bytes / 4;
+  (void)hipGetLastError();
+  fill_zero_kernel<<<(unsigned)((n + 255) / 256), 256, 0, stream>>>(static_cast<int*>(workspace),
+                                                                     n);
+  return hipGetLastError() == hipSuccess ? DLFP_OK : DLFP_EHIP;
+}
+
+extern "C" int dlfp_workspace_error(const void* workspace, int32_t* host_error,
+                                    hipStream_t stream) {
+  if (!workspace || !host_error) return DLFP_EINVAL;
+  if (hipStreamSynchronize(stream) != hipSuccess) return DLFP_EHIP;
+  if (hipMemcpy(host_error, workspace, sizeof(int32_t), hipMemcpyDeviceToHost) != hipSuccess)
+    return DLFP_EHIP;
+  return DLFP_OK;
+}

@@ -1,0 +1,302 @@
+// Host half of libdlfp: packed-batch metadata and work list, the Eq. 2
+// controller, completion timers, status strings.  Device launches live in
+// kv_append.hip and attention_mixed.hip.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <limits>
+#include <vector>
+
+#include "dlfp.h"
+#include "dlfp_internal.h"
+
+namespace {
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
+
+struct Unit {
+  int32_t f[DLFP_WORK_INTS];
+};
+
+}  // namespace
+
+namespace dlfp {
+
+int check_dims(const dlfp_dims* dims, int* group) {
+  if (!dims) return DLFP_EINVAL;
+  if (dims->num_q_heads <= 0 || dims->num_kv_heads <= 0) return DLFP_EINVAL;
+  if (dims->head_dim != DLFP_HEAD_DIM || dims->page_size != DLFP_PAGE_SIZE)
+    return DLFP_EUNSUPPORTED;
+  if (dims->num_q_heads % dims->num_kv_heads) return DLFP_EUNSUPPORTED;
+  const int g = dims->num_q_heads / dims->num_kv_heads;
+  if (g != 1 && g != 2 && g != 4 && g != 8) return DLFP_EUNSUPPORTED;
+  if (group) *group = g;
+  return DLFP_OK;
+}
+
+}  // namespace dlfp
+
+extern "C" {
+
+int dlfp_version(void) { return 100; }
+
+const char* dlfp_status_string(int status) {
+  switch (status) {
+    case DLFP_OK: return "ok";
+    case DLFP_EINVAL: return "invalid argument";
+    case DLFP_ERANGE: return "index out of range";
+    case DLFP_ENOSPC: return "capacity or workspace too small";
+    case DLFP_EHIP: return "HIP runtime error";
+    case DLFP_EUNSUPPORTED: return "unsupported shape";
+    default: return "unknown status";
+  }
+}
+
+// Work-list policy.  Prefill rows are packed token-major into tiles of
+// DLFP_TILE_ROWS rows (DLFP_TILE_ROWS / g tokens, each with its g query heads
+// that share one KV head).  Each tile's visible key range [0, last row's
+// position] and each decoder's range [0, kv_len) is cut into splits; splits of
+// the same rows form a group that the attention launch combines in split
+// order.  Prefill units are ordered KV-head-major so that, with workgroups
+// dealt round-robin over the XCDs, units reading the same KV head share an L2.
+int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int32_t num_seqs,
+                           const int32_t* q_len, const int32_t* kv_len,
+                           const int32_t* block_table, int32_t max_blocks, int32_t num_blocks,
+                           dlfp_meta* meta) {
+  int g = 0;
+  int st = dlfp::check_dims(dims, &g);
+  if (st != DLFP_OK) return st;
+  if (!meta || num_seqs < 0) return DLFP_EINVAL;
+  if (num_seqs > 0 && (!q_len || !kv_len || !block_table || max_blocks <= 0)) return DLFP_EINVAL;
+  if (num_blocks < 0) return DLFP_EINVAL;
+  dlfp_tuning tn = {0, 0, 0};
+  if (tuning) tn = *tuning;
+  if (tn.decode_split_tokens < 0 || tn.decode_split_tokens % DLFP_PAGE_SIZE) return DLFP_EINVAL;
+  if (tn.prefill_split_tokens < 0 || tn.prefill_split_tokens % 64) return DLFP_EINVAL;
+  if (tn.target_units < 0) return DLFP_EINVAL;
+  const int64_t target = tn.target_units ? tn.target_units : 4096;
+  const int hkv = dims->num_kv_heads;
+  const int tile_tokens = DLFP_TILE_ROWS / g;
+
+  // Validate sequences and the pages they use.
+  int64_t tokens = 0, dec_keys = 0, pre_keys = 0;
+  for (int s = 0; s < num_seqs; ++s) {
+    const int32_t ql = q_len[s], kl = kv_len[s];
+    if (ql < 1 || kl < ql) return DLFP_EINVAL;
+    const int64_t pages = ceil_div(kl, DLFP_PAGE_SIZE);
+    if (pages > max_blocks) return DLFP_ERANGE;
+    const int32_t* row = block_table + (int64_t)s * max_blocks;
+    for (int64_t p = 0; p < pages; ++p)
+      if (row[p] < 0 || row[p] >= num_blocks) return DLFP_ERANGE;
+    if ((int64_t)num_blocks * DLFP_PAGE_SIZE > std::numeric_limits<int32_t>::max())
+      return DLFP_ERANGE;
+    tokens += ql;
+    if (ql == 1) {
+      dec_keys += (int64_t)kl * hkv;
+    } else {
+      const int64_t pos0 = kl - ql;
+      for (int64_t t0 = 0; t0 < ql; t0 += tile_tokens) {
+        const int64_t nt = std::min<int64_t>(tile_tokens, ql - t0);
+        pre_keys += (pos0 + t0 + nt) * hkv;
+      }
+    }
+  }
+  if (tokens > std::numeric_limits<int32_t>::max()) return DLFP_ERANGE;
+
+  // Split sizes.
+  int64_t split_d = tn.decode_split_tokens;
+  if (!split_d) split_d = std::clamp<int64_t>(round_up(std::max<int64_t>(1, ceil_div(dec_keys, target)), 16), 128, 16384);
+  int64_t split_p = tn.prefill_split_tokens;
+  if (!split_p) split_p = std::max<int64_t>(1024, round_up(std::max<int64_t>(1, ceil_div(pre_keys, std::max<int64_t>(1, target / 4))), 64));
+
+  // Build units: prefill (KV-head-major), then decode.
+  std::vector<Unit> units;
+  int32_t groups = 0;
+  std::vector<int64_t> group_rows;  // rows of each group
+  auto emit = [&](int s, int kh, int64_t t0, int64_t nt, int64_t kend, int64_t split, int kind) {
+    const int64_t nsp = ceil_div(kend, split);
+    const int32_t grp = nsp > 1 ? groups++ : -1;
+    if (nsp > 1) group_rows.push_back(nt * g);
+    for (int64_t j = 0; j < nsp; ++j) {
+      Unit u;
+      std::memset(&u, 0, sizeof(u));
+      u.f[DLFP_W_SEQ] = s;
+      u.f[DLFP_W_KVHEAD] = kh;
+      u.f[DLFP_W_QTOK0] = (int32_t)t0;
+      u.f[DLFP_W_QNTOK] = (int32_t)nt;
+      u.f[DLFP_W_KVBEGIN] = (int32_t)(j * split);
+      u.f[DLFP_W_KVEND] = (int32_t)std::min(kend, (j + 1) * split);
+      u.f[DLFP_W_GROUP] = grp;
+      u.f[DLFP_W_SPLIT] = (int32_t)j;
+      u.f[DLFP_W_NSPLITS] = (int32_t)nsp;
+      u.f[DLFP_W_KIND] = kind;
+      units.push_back(u);
+    }
+  };
+  for (int kh = 0; kh < hkv; ++kh)
+    for (int s = 0; s < num_seqs; ++s) {
+      if (q_len[s] == 1) continue;
+      const int64_t pos0 = kv_len[s] - q_len[s];
+      for (int64_t t0 = 0; t0 < q_len[s]; t0 += tile_tokens) {
+        const int64_t nt = std::min<int64_t>(tile_tokens, q_len[s] - t0);
+        emit(s, kh, t0, nt, pos0 + t0 + nt, split_p, DLFP_KIND_PREFILL);
+      }
+    }
+  const int64_t num_prefill = (int64_t)units.size();
+  for (int s = 0; s < num_seqs; ++s) {
+    if (q_len[s] != 1) continue;
+    for (int kh = 0; kh < hkv; ++kh) emit(s, kh, 0, 1, kv_len[s], split_d, DLFP_KIND_DECODE);
+  }
+  if ((int64_t)units.size() > std::numeric_limits<int32_t>::max() / DLFP_WORK_INTS)
+    return DLFP_ERANGE;
+  if (groups > DLFP_MAX_GROUPS) return DLFP_ERANGE;
+
+  // Workspace: header, the fixed counter region, then partial slots.
+  const int64_t partial_base_bytes = DLFP_WORKSPACE_PARTIALS;
+  std::vector<int64_t> group_off(groups, 0);
+  int64_t off = partial_base_bytes / 4;
+  {
+    // assign in order of first appearance (units are grouped contiguously)
+    std::vector<int64_t> seen(groups, -1);
+    for (const Unit& u : units) {
+      const int32_t grp = u.f[DLFP_W_GROUP];
+      if (grp < 0 || seen[grp] >= 0) continue;
+      seen[grp] = off;
+      group_off[grp] = off;
+      off += (int64_t)u.f[DLFP_W_NSPLITS] * group_rows[grp] * (DLFP_HEAD_DIM + 2);
+    }
+  }
+  if (off > std::numeric_limits<int32_t>::max()) return DLFP_ERANGE;
+  for (Unit& u : units) {
+    const int32_t grp = u.f[DLFP_W_GROUP];
+    if (grp < 0) continue;
+    const int64_t slot = group_rows[grp] * (DLFP_HEAD_DIM + 2);
+    u.f[DLFP_W_WSGROUP] = (int32_t)group_off[grp];
+    u.f[DLFP_W_WSOFF] = (int32_t)(group_off[grp] + u.f[DLFP_W_SPLIT] * slot);
+  }
+
+  meta->num_seqs = num_seqs;
+  meta->num_tokens = (int32_t)tokens;
+  meta->num_units = (int32_t)units.size();
+  meta->num_prefill_units = (int32_t)num_prefill;
+  meta->num_groups = groups;
+  meta->decode_split_tokens = (int32_t)split_d;
+  meta->prefill_split_tokens = (int32_t)split_p;
+  meta->workspace_bytes = std::max<int64_t>(off * 4, partial_base_bytes);
+  if (meta->cap_seqs < num_seqs || meta->cap_tokens < tokens ||
+      meta->cap_work < (int64_t)units.size())
+    return DLFP_ENOSPC;
+  if ((num_seqs > 0 && (!meta->cu_q || !meta->q_pos0)) || (tokens > 0 && !meta->slot_mapping) ||
+      (!units.empty() && !meta->work))
+    return DLFP_EINVAL;
+  if (meta->cu_q) meta->cu_q[0] = 0;
+  int64_t t = 0;
+  for (int s = 0; s < num_seqs; ++s) {
+    const int32_t pos0 = kv_len[s] - q_len[s];
+    meta->q_pos0[s] = pos0;
+    const int32_t* row = block_table + (int64_t)s * max_blocks;
+    for (int32_t i = 0; i < q_len[s]; ++i) {
+      const int32_t p = pos0 + i;
+      meta->slot_mapping[t++] = row[p / DLFP_PAGE_SIZE] * DLFP_PAGE_SIZE + p % DLFP_PAGE_SIZE;
+    }
+    meta->cu_q[s + 1] = (int32_t)t;
+  }
+  for (size_t u = 0; u < units.size(); ++u)
+    std::memcpy(meta->work + u * DLFP_WORK_INTS, units[u].f, sizeof(units[u].f));
+  return DLFP_OK;
+}
+
+int dlfp_controller_init(dlfp_controller* ctrl, double target_ms, int32_t c_initial,
+                         int32_t c_min, int32_t c_max, int32_t quantum) {
+  if (!ctrl) return DLFP_EINVAL;
+  if (!(std::isfinite(target_ms) && target_ms > 0.0)) return DLFP_EINVAL;
+  if (!(0 < c_min && c_min <= c_initial && c_initial <= c_max) || quantum <= 0)
+    return DLFP_EINVAL;
+  ctrl->target_ms = target_ms;
+  ctrl->c_initial = c_initial;
+  ctrl->c_min = c_min;
+  ctrl->c_max = c_max;
+  ctrl->quantum = quantum;
+  ctrl->cap = c_initial;
+  return DLFP_OK;
+}
+
+// Eq. 2 (Sec. 3.1).  floor_quantum(x) = quantum * floor(x / quantum) in
+// double precision, then clamp to [c_min, c_max].
+int dlfp_controller_step(dlfp_controller* ctrl, int32_t num_decoding_next,
+                         int32_t last_was_guarded, double observed_ms, int32_t* next_cap) {
+  if (!ctrl || !next_cap || num_decoding_next < 0) return DLFP_EINVAL;
+  if (last_was_guarded) {
+    if (!(std::isfinite(observed_ms) && observed_ms > 0.0)) return DLFP_EINVAL;
+    const double x = (double)ctrl->cap * ctrl->target_ms / observed_ms;
+    const double q = std::floor(x / ctrl->quantum);
+    int64_t c;
+    if (!(q < (double)std::numeric_limits<int32_t>::max()))
+      c = ctrl->c_max;
+    else
+      c = (int64_t)q * ctrl->quantum;
+    c = std::min<int64_t>(std::max<int64_t>(c, ctrl->c_min), ctrl->c_max);
+    ctrl->cap = (int32_t)c;
+  }
+  if (num_decoding_next == 0) {
+    ctrl->cap = ctrl->c_initial;
+    *next_cap = -1;
+  } else {
+    *next_cap = ctrl->cap;
+  }
+  return DLFP_OK;
+}
+
+struct dlfp_timer_s {
+  hipEvent_t start, stop;
+};
+
+int dlfp_timer_create(dlfp_timer* timer) {
+  if (!timer) return DLFP_EINVAL;
+  dlfp_timer t = new (std::nothrow) dlfp_timer_s;
+  if (!t) return DLFP_EINVAL;
+  if (hipEventCreate(&t->start) != hipSuccess) {
+    delete t;
+    return DLFP_EHIP;
+  }
+  if (hipEventCreate(&t->stop) != hipSuccess) {
+    (void)hipEventDestroy(t->start);
+    delete t;
+    return DLFP_EHIP;
+  }
+  *timer = t;
+  return DLFP_OK;
+}
+
+int dlfp_timer_destroy(dlfp_timer timer) {
+  if (!timer) return DLFP_EINVAL;
+  const bool ok = hipEventDestroy(timer->start) == hipSuccess &&
+                  hipEventDestroy(timer->stop) == hipSuccess;
+  delete timer;
+  return ok ? DLFP_OK : DLFP_EHIP;
+}
+
+int dlfp_timer_start(dlfp_timer timer, hipStream_t stream) {
+  if (!timer) return DLFP_EINVAL;
+  return hipEventRecord(timer->start, stream) == hipSuccess ? DLFP_OK : DLFP_EHIP;
+}
+
+int dlfp_timer_stop(dlfp_timer timer, hipStream_t stream) {
+  if (!timer) return DLFP_EINVAL;
+  return hipEventRecord(timer->stop, stream) == hipSuccess ? DLFP_OK : DLFP_EHIP;
+}
+
+int dlfp_timer_elapsed_ms(dlfp_timer timer, double* ms) {
+  if (!timer || !ms) return DLFP_EINVAL;
+  if (hipEventSynchronize(timer->stop) != hipSuccess) return DLFP_EHIP;
+  float f = 0.f;
+  if (hipEventElapsedTime(&f, timer->start, timer->stop) != hipSuccess) return DLFP_EHIP;
+  *ms = f;
+  return DLFP_OK;
+}
+
+}  // extern "C"

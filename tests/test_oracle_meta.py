@@ -52,7 +52,7 @@ def _valid_list():
     seq 1: decoder with kv 40 split into [0,32) and [32,40).  One KV head."""
     g, rows_t = 2, 64
     slot = lambda rows: rows * (128 + 2)
-    base = 64  # counters for 2 groups padded to 256 bytes = 64 floats
+    base = (256 + 4 * 65536) // 4  # header + fixed counter region, in floats
     units = [
         _unit(0, 0, 0, 64, 0, 48, grp=0, split=0, nsp=2, wsoff=base, wsgrp=base),
         _unit(0, 0, 0, 64, 48, 94, grp=0, split=1, nsp=2, wsoff=base + slot(128), wsgrp=base),
