@@ -58,6 +58,10 @@ extern "C" {
 #define DLFP_PAGE_SIZE 16
 /* Query rows (tokens x grouped query heads) held by one prefill unit. */
 #define DLFP_TILE_ROWS 128
+/* Longest key range of one work unit; the builder splits longer ranges.  A
+ * unit keeps its slice of the block table in LDS, which bounds these. */
+#define DLFP_MAX_DECODE_UNIT_KEYS 8192
+#define DLFP_MAX_PREFILL_UNIT_KEYS 32768
 /* int32 fields per work unit (see dlfp_build_varlen_meta). */
 #define DLFP_WORK_INTS 16
 /* Workspace layout: a 256-byte header (word 0 = error flag), then a fixed
@@ -89,8 +93,10 @@ typedef struct {
  * the built-in policy, which sizes splits so the launch has about
  * target_units units of work. */
 typedef struct {
-  int32_t decode_split_tokens;   /* keys per decode unit; 0 = auto, else a multiple of 16 */
-  int32_t prefill_split_tokens;  /* keys per prefill unit; 0 = auto, else a multiple of 64 */
+  int32_t decode_split_tokens;   /* keys per decode unit; 0 = auto, else a multiple of 16,
+                                    at most DLFP_MAX_DECODE_UNIT_KEYS */
+  int32_t prefill_split_tokens;  /* keys per prefill unit; 0 = auto, else a multiple of 64,
+                                    at most DLFP_MAX_PREFILL_UNIT_KEYS */
   int32_t target_units;          /* auto policy target; 0 = 4096 */
 } dlfp_tuning;
 
@@ -123,7 +129,9 @@ enum {
   DLFP_W_GROUP = 6,    /* split group, -1 when the unit alone covers its rows */
   DLFP_W_SPLIT = 7,    /* index of this split within the group */
   DLFP_W_NSPLITS = 8,  /* splits in the group */
-  DLFP_W_WSOFF = 9,    /* float offset of this unit's partial result in the workspace */
+  DLFP_W_WSOFF = 9,    /* float offset of this unit's partial result in the workspace; a
+                          slot holds O[rows][128], m[rows], l[rows] (rows = tokens x g),
+                          padded to a multiple of 64 floats */
   DLFP_W_WSGROUP = 10, /* float offset of the group's split 0 partial */
   DLFP_W_KIND = 11     /* DLFP_KIND_PREFILL or DLFP_KIND_DECODE */
 };

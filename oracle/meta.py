@@ -115,7 +115,7 @@ def check_work_list(work: np.ndarray, num_prefill: int, q_len: Sequence[int],
                 fail(f"unit {u}: group {grp} out of range")
             groups.setdefault(grp, []).append(it)
             rows = nt * g
-            slot_floats = rows * (HEAD_DIM + 2)
+            slot_floats = (rows * (HEAD_DIM + 2) + 63) // 64 * 64   # padded to 256 bytes
             if wsoff != wsgrp + split * slot_floats:
                 fail(f"unit {u}: partial slot offset")
             if wsgrp < partial_base:

@@ -57,8 +57,13 @@ constexpr int PAGE_ELEMS = PAGE * D;          // bf16 elements per (block, head)
 constexpr int KV_TILE = 64;                   // keys per prefill tile (4 pages)
 constexpr int THREADS = 256;
 constexpr int STAGE_BYTES = 2 * KV_TILE * D * 2;   // K tile + V^T tile
-constexpr int LDS_BYTES = 2 * STAGE_BYTES;         // double buffered: 64 KiB
-constexpr int DEC_WAVE_LDS = 2 * PAGE_ELEMS * 2 + 16 * 16 * 2;  // K page, V page, p buffer
+constexpr int PRE_PTAB = DLFP_MAX_PREFILL_UNIT_KEYS / PAGE;  // block ids of one prefill unit
+constexpr int LDS_BYTES = 2 * STAGE_BYTES + PRE_PTAB * 4;    // 64 KiB of stages + 8 KiB
+constexpr int DEC_PTAB = DLFP_MAX_DECODE_UNIT_KEYS / PAGE;   // block ids of one decode unit
+// Per decode wave: K page, V page, probability buffer, block ids, and (for
+// g = 8) the query of the group.
+constexpr int DEC_Q_LDS = 8 * D * 2;
+constexpr int DEC_WAVE_LDS = 2 * PAGE_ELEMS * 2 + 16 * 16 * 2 + DEC_PTAB * 4 + DEC_Q_LDS;
 constexpr float NEG_BIG = -1.0e30f;
 constexpr float LOG2E = 1.4426950408889634f;
 
@@ -123,12 +128,77 @@ __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+__device__ __forceinline__ int* group_counter_ptr(float* ws, int grp) {
+  return reinterpret_cast<int*>(reinterpret_cast<char*>(ws) + DLFP_WORKSPACE_HEADER) + grp;
+}
+
 __device__ __forceinline__ void raise_error(float* ws) {
   __hip_atomic_store(reinterpret_cast<int*>(ws), 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// Split-K partial results cross workgroups (and XCDs, whose L2s are not
+// coherent with each other).  They are written with device-coherent stores
+// (the sc1 policy: written through to the device coherence point) and read
+// back with device-coherent loads (which do not return stale L2 lines), both
+// through a buffer resource bounded to the group's slots.  Before a unit
+// bumps its group counter it waits until all its vector-memory operations,
+// stores included, have completed; the last arriver issues its loads only
+// after the counter read has returned.  This orders the exchange without
+// writing back or invalidating whole L2 caches per unit.
+constexpr int CPOL_SC1 = 16;  // cache-policy bit: coherent at device scope
+
+struct Slots {
+  __amdgpu_buffer_rsrc_t r;
+};
+
+__device__ __forceinline__ Slots group_slots(float* ws, int group_off, int nsplits,
+                                             int slot_floats) {
+  return Slots{__builtin_amdgcn_make_buffer_rsrc(ws + group_off, 0, nsplits * slot_floats * 4,
+                                                 0x00020000)};
+}
+__device__ __forceinline__ void pstore4(Slots s, int float_off, f32x4_t v) {
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, v), s.r, float_off * 4, 0,
+                                         CPOL_SC1);
+}
+__device__ __forceinline__ void pstore2(Slots s, int float_off, f32x2_t v) {
+  __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2_t, v), s.r, float_off * 4, 0,
+                                        CPOL_SC1);
+}
+__device__ __forceinline__ void pstore1(Slots s, int float_off, float v) {
+  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), s.r, float_off * 4, 0,
+                                        CPOL_SC1);
+}
+__device__ __forceinline__ f32x4_t pload4(Slots s, int float_off) {
+  return __builtin_bit_cast(f32x4_t,
+                            __builtin_amdgcn_raw_buffer_load_b128(s.r, float_off * 4, 0, CPOL_SC1));
+}
+__device__ __forceinline__ f32x2_t pload2(Slots s, int float_off) {
+  return __builtin_bit_cast(f32x2_t,
+                            __builtin_amdgcn_raw_buffer_load_b64(s.r, float_off * 4, 0, CPOL_SC1));
+}
+__device__ __forceinline__ float pload1(Slots s, int float_off) {
+  return __builtin_bit_cast(float,
+                            __builtin_amdgcn_raw_buffer_load_b32(s.r, float_off * 4, 0, CPOL_SC1));
+}
+// Floats per partial slot: O[rows][128], m[rows], l[rows], padded to 256 bytes.
+__device__ __forceinline__ int slot_floats_for(int rows) {
+  return (rows * (D + 2) + 63) / 64 * 64;
+}
+// Wait for every outstanding vector-memory operation of this wave (on gfx9 the
+// vector-memory counter covers stores) and keep the compiler from moving
+// memory operations across the wait.
+__device__ __forceinline__ void wait_memory_complete() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0), expcnt and lgkmcnt unconstrained
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+__device__ __forceinline__ int arrive(float* ws, int grp) {
+  return __hip_atomic_fetch_add(group_counter_ptr(ws, grp), 1, __ATOMIC_RELAXED,
+                                __HIP_MEMORY_SCOPE_AGENT);
+}
+
 __device__ __forceinline__ int* group_counter(float* ws, int grp) {
-  return reinterpret_cast<int*>(reinterpret_cast<char*>(ws) + DLFP_WORKSPACE_HEADER) + grp;
+  return group_counter_ptr(ws, grp);
 }
 
 // Workgroups are dealt round-robin over the 8 XCDs; map them so that each XCD
@@ -180,24 +250,23 @@ struct Stage {
   u32x4_t c[8];
 };
 
-__device__ __forceinline__ void load_stage(Stage& st, const Args& a, const int32_t* bt, int kh,
-                                           int k0, int ke, int tid) {
+// ptab: the unit's block ids in LDS, ptab[i] = block of page kb / 16 + i.
+__device__ __forceinline__ void load_stage(Stage& st, const Args& a, const int32_t* ptab, int kh,
+                                           int kb, int k0, int ke, int tid) {
+  // Straight-line on purpose: pages past the unit's last key re-read its last
+  // page (an L2 hit; every key there is masked), and a block id outside the
+  // pool is replaced by block 0 after raising the error word.  Block ids come
+  // from LDS, so waiting for them never waits for the tile loads in flight.
+  const int last_page = (ke - 1) / PAGE;
 #pragma unroll
   for (int pg = 0; pg < 4; ++pg) {
-    const int key0 = k0 + pg * PAGE;
-    u32x4_t kv = {0, 0, 0, 0}, vv = {0, 0, 0, 0};
-    if (key0 < ke) {
-      const int blk = bt[key0 / PAGE];
-      if ((unsigned)blk < (unsigned)a.num_blocks) {
-        const int64_t base = ((int64_t)blk * a.hkv + kh) * PAGE_ELEMS + tid * 8;
-        kv = *reinterpret_cast<const u32x4_t*>(a.kc + base);
-        vv = *reinterpret_cast<const u32x4_t*>(a.vc + base);
-      } else if (tid == 0) {
-        raise_error(a.ws);
-      }
-    }
-    st.c[pg] = kv;
-    st.c[4 + pg] = vv;
+    const int page = min(k0 / PAGE + pg, last_page);
+    const int raw = ptab[page - kb / PAGE];
+    const bool ok = (unsigned)raw < (unsigned)a.num_blocks;
+    if (!ok && tid == 0) raise_error(a.ws);
+    const int64_t base = ((int64_t)(ok ? raw : 0) * a.hkv + kh) * PAGE_ELEMS + tid * 8;
+    st.c[pg] = *reinterpret_cast<const u32x4_t*>(a.kc + base);
+    st.c[4 + pg] = *reinterpret_cast<const u32x4_t*>(a.vc + base);
   }
 }
 
@@ -245,16 +314,15 @@ __device__ void prefill_unit(const Args& a, const int32_t* it, char* smem, int* 
   const int wave_lim_min = min(pos0 + t0 + wave_tok0 + 1, ke);
 
   // Q^T as the B operand: lane holds dims [16kk + 8hi, +8) of its row.
+  // Rows past the unit's tokens load the first row's query; they are never stored.
   bf16x8_t qf[8];
   {
     const int64_t qrow = ((int64_t)(q0 + t0 + (row_ok ? tr : 0)) * a.hq + kh * G + hh) * D;
 #pragma unroll
-    for (int kk = 0; kk < 8; ++kk) {
-      u32x4_t v = {0, 0, 0, 0};
-      if (row_ok) v = *reinterpret_cast<const u32x4_t*>(a.q + qrow + 16 * kk + 8 * hi);
-      qf[kk] = __builtin_bit_cast(bf16x8_t, v);
-    }
+    for (int kk = 0; kk < 8; ++kk)
+      qf[kk] = *reinterpret_cast<const bf16x8_t*>(a.q + qrow + 16 * kk + 8 * hi);
   }
+  wait_memory_complete();  // queries resident before the KV pipeline starts
 
   float m_run = NEG_BIG, l_run = 0.f;
   f32x16_t o[4];
@@ -262,15 +330,21 @@ __device__ void prefill_unit(const Args& a, const int32_t* it, char* smem, int* 
   for (int mb = 0; mb < 4; ++mb) o[mb] = f32x16_t{};
 
   const int ntiles = (ke - kb + KV_TILE - 1) / KV_TILE;
+  // The unit's slice of the block table goes to LDS first.
+  int32_t* ptab = reinterpret_cast<int32_t*>(smem + 2 * STAGE_BYTES);
+  const int n_pages = (ke + PAGE - 1) / PAGE - kb / PAGE;
+  for (int i = tid; i < n_pages; i += THREADS) ptab[i] = bt[kb / PAGE + i];
+  wait_memory_complete();
+  __syncthreads();
   Stage st;
-  load_stage(st, a, bt, kh, kb, ke, tid);
+  load_stage(st, a, ptab, kh, kb, kb, ke, tid);
   store_stage(st, smem, tid, kb, ke);
   __syncthreads();
 
   for (int ti = 0; ti < ntiles; ++ti) {
     const int k0 = kb + ti * KV_TILE;
     const bool more = ti + 1 < ntiles;
-    if (more) load_stage(st, a, bt, kh, k0 + KV_TILE, ke, tid);
+    if (more) load_stage(st, a, ptab, kh, kb, k0 + KV_TILE, ke, tid);
     const char* buf = smem + (ti & 1) * STAGE_BYTES;
 
     if (wave_active) {
@@ -323,8 +397,10 @@ __device__ void prefill_unit(const Args& a, const int32_t* it, char* smem, int* 
         pf[kk] = __builtin_bit_cast(bf16x8_t, pk);
       }
       l_run = l_run * alpha + psum;
+      if (__builtin_amdgcn_ballot_w64(alpha != 1.f)) {
 #pragma unroll
-      for (int mb = 0; mb < 4; ++mb) o[mb] *= alpha;
+        for (int mb = 0; mb < 4; ++mb) o[mb] *= alpha;
+      }
       // O^T += V^T P^T, one 16-key page per k-step.
       const char* vbuf = buf + KV_TILE * D * 2;
 #pragma unroll
@@ -365,51 +441,58 @@ __device__ void prefill_unit(const Args& a, const int32_t* it, char* smem, int* 
   }
 
   // Partial result: O[rows][128], then m[rows], then l[rows].
-  float* slot = a.ws + it[DLFP_W_WSOFF];
+  const int slot_floats = slot_floats_for(rows);
+  const Slots sl = group_slots(a.ws, it[DLFP_W_WSGROUP], nsplits, slot_floats);
+  const int my = it[DLFP_W_SPLIT] * slot_floats;
   if (row_ok) {
 #pragma unroll
     for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
       for (int g4 = 0; g4 < 4; ++g4) {
-        f32x4_t v = {o[mb][4 * g4], o[mb][4 * g4 + 1], o[mb][4 * g4 + 2], o[mb][4 * g4 + 3]};
-        *reinterpret_cast<f32x4_t*>(slot + r * D + mb * 32 + 8 * g4 + 4 * hi) = v;
+        const f32x4_t v = {o[mb][4 * g4], o[mb][4 * g4 + 1], o[mb][4 * g4 + 2],
+                           o[mb][4 * g4 + 3]};
+        pstore4(sl, my + r * D + mb * 32 + 8 * g4 + 4 * hi, v);
       }
     if (hi == 0) {
-      slot[rows * D + r] = m_run;
-      slot[rows * D + rows + r] = l_run;
+      pstore1(sl, my + rows * D + r, m_run);
+      pstore1(sl, my + rows * D + rows + r, l_run);
     }
   }
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-  __syncthreads();
+  wait_memory_complete();
+  __syncthreads();  // every wave of the unit has completed its stores
   const int grp = it[DLFP_W_GROUP];
-  if (tid == 0) {
-    const int old = __hip_atomic_fetch_add(group_counter(a.ws, grp), 1, __ATOMIC_ACQ_REL,
-                                           __HIP_MEMORY_SCOPE_AGENT);
-    *flag = old == nsplits - 1;
-  }
+  if (tid == 0) *flag = arrive(a.ws, grp) == nsplits - 1;
   __syncthreads();
   if (!*flag) return;
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
 
-  // Last arriver: merge every split of the group in split order.
-  const float* g0 = a.ws + it[DLFP_W_WSGROUP];
-  const int slot_floats = rows * (D + 2);
-  for (int f = tid; f < rows * (D / 4); f += THREADS) {
-    const int row = f / (D / 4), c4 = f % (D / 4);
+  // Last arriver: merge every split of the group in split order.  Four
+  // threads per row, 32 dims each, two passes over the rows; the loads of a
+  // split are independent of each other.
+  for (int row = tid >> 2; row < rows; row += THREADS / 4) {
+    const int quarter = tid & 3;
     float mmax = NEG_BIG;
-    for (int j = 0; j < nsplits; ++j) mmax = fmaxf(mmax, g0[j * slot_floats + rows * D + row]);
+    for (int j = 0; j < nsplits; ++j)
+      mmax = fmaxf(mmax, pload1(sl, j * slot_floats + rows * D + row));
     float lsum = 0.f;
-    f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+    f32x4_t acc[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     for (int j = 0; j < nsplits; ++j) {
-      const float* sj = g0 + j * slot_floats;
-      const float w = fexp2(sj[rows * D + row] - mmax);
-      lsum += w * sj[rows * D + rows + row];
-      acc += w * *reinterpret_cast<const f32x4_t*>(sj + row * D + 4 * c4);
+      const int base = j * slot_floats;
+      const float w = fexp2(pload1(sl, base + rows * D + row) - mmax);
+      lsum += w * pload1(sl, base + rows * D + rows + row);
+      f32x4_t t[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) t[i] = pload4(sl, base + row * D + quarter * 32 + 4 * i);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) acc[i] += w * t[i];
     }
     const float inv = 1.f / lsum;
     const int trow = row / G, hrow = row % G;
-    const int64_t orow = ((int64_t)(q0 + t0 + trow) * a.hq + kh * G + hrow) * D;
-    store4(a, orow + 4 * c4, acc[0] * inv, acc[1] * inv, acc[2] * inv, acc[3] * inv);
+    const int64_t orow = ((int64_t)(q0 + t0 + trow) * a.hq + kh * G + hrow) * D + quarter * 32;
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+      store4(a, orow + 4 * i, acc[i][0] * inv, acc[i][1] * inv, acc[i][2] * inv, acc[i][3] * inv);
   }
   if (tid == 0)
     __hip_atomic_store(group_counter(a.ws, grp), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -432,17 +515,34 @@ __device__ void decode_unit(const Args& a, const int32_t* it, char* wl) {
   char* kl = wl;
   char* vl = wl + PAGE_ELEMS * 2;
   uint16_t* pbuf = reinterpret_cast<uint16_t*>(wl + 2 * PAGE_ELEMS * 2);
+  int32_t* ptab = reinterpret_cast<int32_t*>(wl + 2 * PAGE_ELEMS * 2 + 16 * 16 * 2);
 
-  // Query of the g heads: lane holds dims [8c, 8c + 8) and [64 + 8c, 64 + 8c + 8).
-  u32x4_t qa[G], qb[G];
+  // Query of the g heads: lane uses dims [8c, 8c + 8) and [64 + 8c, 64 + 8c + 8).
+  // Up to g = 4 they stay in registers; for g = 8 they live in the wave's LDS
+  // slice (each read is an 8-address broadcast) to leave registers for the
+  // page pipeline.
+  constexpr bool Q_IN_LDS = G >= 8;
+  constexpr int QR = Q_IN_LDS ? 1 : G;
+  u32x4_t qa[QR], qb[QR];
+  uint16_t* qlds = reinterpret_cast<uint16_t*>(wl + 2 * PAGE_ELEMS * 2 + 16 * 16 * 2 + DEC_PTAB * 4);
   {
     const uint16_t* qp = a.q + ((int64_t)tok * a.hq + kh * G) * D;
+    if constexpr (Q_IN_LDS) {
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
-      qa[h] = *reinterpret_cast<const u32x4_t*>(qp + h * D + 8 * c);
-      qb[h] = *reinterpret_cast<const u32x4_t*>(qp + h * D + 64 + 8 * c);
+      for (int i = lane; i < G * D / 8; i += 64)
+        *reinterpret_cast<u32x4_t*>(qlds + 8 * i) = *reinterpret_cast<const u32x4_t*>(qp + 8 * i);
+    } else {
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        qa[h] = *reinterpret_cast<const u32x4_t*>(qp + h * D + 8 * c);
+        qb[h] = *reinterpret_cast<const u32x4_t*>(qp + h * D + 64 + 8 * c);
+      }
     }
   }
+  const int p_begin = kb / PAGE, p_end = (ke + PAGE - 1) / PAGE;
+  for (int i = lane; i < p_end - p_begin; i += 64) ptab[i] = bt[p_begin + i];
+  wait_memory_complete();  // queries and block ids resident before the page pipeline starts
+  wave_sync();
   float m[G], l[G], o0[G], o1[G];
 #pragma unroll
   for (int h = 0; h < G; ++h) {
@@ -452,84 +552,95 @@ __device__ void decode_unit(const Args& a, const int32_t* it, char* wl) {
     o1[h] = 0.f;
   }
 
-  const int p_begin = kb / PAGE, p_end = (ke + PAGE - 1) / PAGE;
-  u32x4_t fk[4], fv[4];
-  auto fetch = [&](int p) {
-    const int blk = bt[p];
-    if ((unsigned)blk < (unsigned)a.num_blocks) {
-      const int64_t base = ((int64_t)blk * a.hkv + kh) * PAGE_ELEMS;
+  // NSLOT register buffers rotate: while one page is consumed from LDS the
+  // next NSLOT are in flight (g = 8 keeps one, for registers).  The loop is
+  // straight-line: a page index past the unit's last page re-reads that page
+  // (an L2 hit) and every key in it is masked, and a block id outside the
+  // pool is replaced by block 0 after raising the error word, so the compiler
+  // can keep the prefetch in flight.
+  constexpr int NSLOT = G >= 8 ? 1 : 2;
+  u32x4_t fk[NSLOT][4], fv[NSLOT][4];
+  auto fetch = [&](u32x4_t* k4, u32x4_t* v4, int p) {
+    const int raw = ptab[min(p, p_end - 1) - p_begin];
+    const bool ok = (unsigned)raw < (unsigned)a.num_blocks;
+    if (!ok && lane == 0) raise_error(a.ws);
+    const int64_t base = ((int64_t)(ok ? raw : 0) * a.hkv + kh) * PAGE_ELEMS;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        fk[j] = *reinterpret_cast<const u32x4_t*>(a.kc + base + (64 * j + lane) * 8);
-        fv[j] = *reinterpret_cast<const u32x4_t*>(a.vc + base + (64 * j + lane) * 8);
-      }
-    } else {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        fk[j] = u32x4_t{0, 0, 0, 0};
-        fv[j] = u32x4_t{0, 0, 0, 0};
-      }
-      if (lane == 0) raise_error(a.ws);
+    for (int j = 0; j < 4; ++j) {
+      k4[j] = *reinterpret_cast<const u32x4_t*>(a.kc + base + (64 * j + lane) * 8);
+      v4[j] = *reinterpret_cast<const u32x4_t*>(a.vc + base + (64 * j + lane) * 8);
     }
   };
-  fetch(p_begin);
 
-  for (int p = p_begin; p < p_end; ++p) {
-    // Stage the fetched page in LDS.
+  auto process = [&](u32x4_t* k4, u32x4_t* v4, int p) {
+    // Stage the fetched page in LDS, then refill the ring slot.
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int q = 64 * j + lane;
       const int R = q >> 4, x = q & 15;
-      *reinterpret_cast<u32x4_t*>(kl + R * 256 + ((x ^ ((R & 1) << 3)) << 4)) = fk[j];
+      *reinterpret_cast<u32x4_t*>(kl + R * 256 + ((x ^ ((R & 1) << 3)) << 4)) = k4[j];
       const int rg = q >> 2, si = q & 3;
-      u32x4_t v = fv[j];
+      u32x4_t v = v4[j];
       const int key0 = p * PAGE + 8 * (si & 1);
       if (key0 + 8 > ke) v = mask_keys(v, key0, ke);
       *reinterpret_cast<u32x4_t*>(vl + rg * 64 + (((si + (rg >> 2)) & 3) << 4)) = v;
     }
-    if (p + 1 < p_end) fetch(p + 1);
+    fetch(k4, v4, p + NSLOT);
     wave_sync();  // staged page visible to every lane
 
-    // Scores of keys 8 st + kg, reduced over the 8 lanes of each key.
-    float sc[2][G];
+    // Keys 8 st + kg of the page (st = 0, 1): each lane holds 16 dims of both.
+    u32x4_t kv[2][2];
 #pragma unroll
     for (int st = 0; st < 2; ++st) {
       const int R = 8 * st + kg;
-      const u32x4_t k0v =
-          *reinterpret_cast<const u32x4_t*>(kl + R * 256 + ((c ^ ((R & 1) << 3)) << 4));
-      const u32x4_t k1v =
+      kv[st][0] = *reinterpret_cast<const u32x4_t*>(kl + R * 256 + ((c ^ ((R & 1) << 3)) << 4));
+      kv[st][1] =
           *reinterpret_cast<const u32x4_t*>(kl + R * 256 + (((c + 8) ^ ((R & 1) << 3)) << 4));
-      const bool valid = p * PAGE + R < ke;
+    }
+    const bool valid0 = p * PAGE + kg < ke, valid1 = p * PAGE + 8 + kg < ke;
+    // One head at a time: scores (dot products summed over the 8 lanes of a
+    // key), online-softmax update, probabilities to LDS, accumulator rescale.
 #pragma unroll
-      for (int h = 0; h < G; ++h) {
+    for (int h = 0; h < G; ++h) {
+      u32x4_t qah, qbh;
+      if constexpr (Q_IN_LDS) {
+        qah = *reinterpret_cast<const u32x4_t*>(qlds + h * D + 8 * c);
+        qbh = *reinterpret_cast<const u32x4_t*>(qlds + h * D + 64 + 8 * c);
+      } else {
+        qah = qa[h];
+        qbh = qb[h];
+      }
+      float sc[2];
+#pragma unroll
+      for (int st = 0; st < 2; ++st) {
         float acc = 0.f;
 #pragma unroll
-        for (int w = 0; w < 4; ++w) acc = dot2(qa[h][w], k0v[w], acc);
+        for (int w = 0; w < 4; ++w) acc = dot2(qah[w], kv[st][0][w], acc);
 #pragma unroll
-        for (int w = 0; w < 4; ++w) acc = dot2(qb[h][w], k1v[w], acc);
+        for (int w = 0; w < 4; ++w) acc = dot2(qbh[w], kv[st][1][w], acc);
         acc += dpp<DPP_XOR1>(acc);
         acc += dpp<DPP_XOR2>(acc);
         acc += dpp<DPP_HALF_MIRROR>(acc);
-        sc[st][h] = valid ? acc * a.scale_log2 : -__builtin_inff();
+        sc[st] = acc * a.scale_log2;
       }
-    }
-    // Online softmax per head.
-    float alpha[G];
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      float mx = fmaxf(sc[0][h], sc[1][h]);
+      sc[0] = valid0 ? sc[0] : -__builtin_inff();
+      sc[1] = valid1 ? sc[1] : -__builtin_inff();
+      float mx = fmaxf(sc[0], sc[1]);
       mx = fmaxf(mx, dpp<DPP_ROR8>(mx));
       mx = fmaxf(mx, shfl_xor(mx, 16));
       mx = fmaxf(mx, shfl_xor(mx, 32));
       const float m_new = fmaxf(m[h], mx);
-      alpha[h] = fexp2(m[h] - m_new);
+      const float alpha = fexp2(m[h] - m_new);
       m[h] = m_new;
-      const float p0 = fexp2(sc[0][h] - m_new), p1 = fexp2(sc[1][h] - m_new);
-      l[h] = l[h] * alpha[h] + (c == 0 ? p0 + p1 : 0.f);
+      const float p0 = fexp2(sc[0] - m_new), p1 = fexp2(sc[1] - m_new);
+      l[h] = l[h] * alpha + (c == 0 ? p0 + p1 : 0.f);
+      o0[h] *= alpha;
+      o1[h] *= alpha;
       if (c == (h & 7)) {
         pbuf[h * 16 + kg] = __builtin_bit_cast(uint16_t, (__bf16)p0);
         pbuf[h * 16 + 8 + kg] = __builtin_bit_cast(uint16_t, (__bf16)p1);
       }
+      if constexpr (G >= 8) __builtin_amdgcn_sched_barrier(0);  // bound live ranges per head
     }
     wave_sync();  // probabilities visible to every lane
     // O += P V: lane owns dims 2 lane and 2 lane + 1.
@@ -541,7 +652,7 @@ __device__ void decode_unit(const Args& a, const int32_t* it, char* wl) {
     for (int h = 0; h < G; ++h) {
       const u32x4_t pp0 = *reinterpret_cast<const u32x4_t*>(pbuf + h * 16);
       const u32x4_t pp1 = *reinterpret_cast<const u32x4_t*>(pbuf + h * 16 + 8);
-      float a0 = o0[h] * alpha[h], a1 = o1[h] * alpha[h];
+      float a0 = o0[h], a1 = o1[h];
 #pragma unroll
       for (int w = 0; w < 4; ++w) {
         a0 = dot2(pp0[w], vr[0][w], a0);
@@ -554,8 +665,16 @@ __device__ void decode_unit(const Args& a, const int32_t* it, char* wl) {
       }
       o0[h] = a0;
       o1[h] = a1;
+      if constexpr (G >= 8) __builtin_amdgcn_sched_barrier(0);
     }
     wave_sync();  // every lane done reading before the next page overwrites LDS
+  };
+
+#pragma unroll
+  for (int j = 0; j < NSLOT; ++j) fetch(fk[j], fv[j], p_begin + j);
+  for (int p = p_begin; p < p_end; p += NSLOT) {
+#pragma unroll
+    for (int j = 0; j < NSLOT; ++j) process(fk[j], fv[j], p + j);  // masked past p_end
   }
 
   // Row sums live on the c == 0 lanes; total them.
@@ -579,40 +698,59 @@ __device__ void decode_unit(const Args& a, const int32_t* it, char* wl) {
   }
 
   // Partial: O[G][128], m[G], l[G].
-  float* slot = a.ws + uniform(it[DLFP_W_WSOFF]);
+  const int slot_floats = slot_floats_for(G);
+  const Slots sl = group_slots(a.ws, uniform(it[DLFP_W_WSGROUP]), nsplits, slot_floats);
+  const int my = uniform(it[DLFP_W_SPLIT]) * slot_floats;
 #pragma unroll
   for (int h = 0; h < G; ++h) {
-    f32x2_t v = {o0[h], o1[h]};
-    *reinterpret_cast<f32x2_t*>(slot + h * D + 2 * lane) = v;
+    pstore2(sl, my + h * D + 2 * lane, f32x2_t{o0[h], o1[h]});
     if (lane == 0) {
-      slot[G * D + h] = m[h];
-      slot[G * D + G + h] = l[h];
+      pstore1(sl, my + G * D + h, m[h]);
+      pstore1(sl, my + G * D + G + h, l[h]);
     }
   }
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
   const int grp = uniform(it[DLFP_W_GROUP]);
+  wait_memory_complete();
   int old = 0;
-  if (lane == 0)
-    old = __hip_atomic_fetch_add(group_counter(a.ws, grp), 1, __ATOMIC_ACQ_REL,
-                                 __HIP_MEMORY_SCOPE_AGENT);
+  if (lane == 0) old = arrive(a.ws, grp);
   old = __shfl(old, 0);
   if (old != nsplits - 1) return;
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
 
-  const float* g0 = a.ws + uniform(it[DLFP_W_WSGROUP]);
-  const int slot_floats = G * (D + 2);
-#pragma unroll
+  // Last arriver: lane j holds split j's statistics (64 splits at a time);
+  // weights reach the accumulating lanes by readlane, in split order.
+#pragma unroll 1
   for (int h = 0; h < G; ++h) {
     float mmax = NEG_BIG;
-    for (int j = 0; j < nsplits; ++j) mmax = fmaxf(mmax, g0[j * slot_floats + G * D + h]);
+    for (int j0 = 0; j0 < nsplits; j0 += 64) {
+      const int j = j0 + lane;
+      float mj = j < nsplits ? pload1(sl, j * slot_floats + G * D + h) : NEG_BIG;
+      mj = fmaxf(mj, shfl_xor(mj, 1));
+      mj = fmaxf(mj, shfl_xor(mj, 2));
+      mj = fmaxf(mj, shfl_xor(mj, 4));
+      mj = fmaxf(mj, shfl_xor(mj, 8));
+      mj = fmaxf(mj, shfl_xor(mj, 16));
+      mj = fmaxf(mj, shfl_xor(mj, 32));
+      mmax = fmaxf(mmax, mj);
+    }
     float lsum = 0.f, acc0 = 0.f, acc1 = 0.f;
-    for (int j = 0; j < nsplits; ++j) {
-      const float* sj = g0 + j * slot_floats;
-      const float w = fexp2(sj[G * D + h] - mmax);
-      lsum += w * sj[G * D + G + h];
-      const f32x2_t v = *reinterpret_cast<const f32x2_t*>(sj + h * D + 2 * lane);
-      acc0 += w * v[0];
-      acc1 += w * v[1];
+    for (int j0 = 0; j0 < nsplits; j0 += 64) {
+      const int j = j0 + lane;
+      float wj = 0.f, lj = 0.f;
+      if (j < nsplits) {
+        wj = fexp2(pload1(sl, j * slot_floats + G * D + h) - mmax);
+        lj = pload1(sl, j * slot_floats + G * D + G + h);
+      }
+      const int n = min(64, nsplits - j0);
+      for (int jj = 0; jj < n; ++jj) {
+        const float w = __builtin_bit_cast(float, __builtin_amdgcn_readlane(
+                                                      __builtin_bit_cast(int, wj), jj));
+        const float lw = __builtin_bit_cast(float, __builtin_amdgcn_readlane(
+                                                       __builtin_bit_cast(int, lj), jj));
+        const f32x2_t v = pload2(sl, (j0 + jj) * slot_floats + h * D + 2 * lane);
+        lsum += w * lw;
+        acc0 += w * v[0];
+        acc1 += w * v[1];
+      }
     }
     const float inv = 1.f / lsum;
     store2(a, obase + h * D, acc0 * inv, acc1 * inv);

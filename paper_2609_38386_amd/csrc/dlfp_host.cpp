@@ -18,6 +18,9 @@ namespace {
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
 
+// Floats of one partial result: O[rows][128], m[rows], l[rows], padded to 256 bytes.
+int64_t slot_floats(int64_t rows) { return round_up(rows * (DLFP_HEAD_DIM + 2), 64); }
+
 struct Unit {
   int32_t f[DLFP_WORK_INTS];
 };
@@ -75,8 +78,12 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
   if (num_blocks < 0) return DLFP_EINVAL;
   dlfp_tuning tn = {0, 0, 0};
   if (tuning) tn = *tuning;
-  if (tn.decode_split_tokens < 0 || tn.decode_split_tokens % DLFP_PAGE_SIZE) return DLFP_EINVAL;
-  if (tn.prefill_split_tokens < 0 || tn.prefill_split_tokens % 64) return DLFP_EINVAL;
+  if (tn.decode_split_tokens < 0 || tn.decode_split_tokens % DLFP_PAGE_SIZE ||
+      tn.decode_split_tokens > DLFP_MAX_DECODE_UNIT_KEYS)
+    return DLFP_EINVAL;
+  if (tn.prefill_split_tokens < 0 || tn.prefill_split_tokens % 64 ||
+      tn.prefill_split_tokens > DLFP_MAX_PREFILL_UNIT_KEYS)
+    return DLFP_EINVAL;
   if (tn.target_units < 0) return DLFP_EINVAL;
   const int64_t target = tn.target_units ? tn.target_units : 4096;
   const int hkv = dims->num_kv_heads;
@@ -109,9 +116,14 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
 
   // Split sizes.
   int64_t split_d = tn.decode_split_tokens;
-  if (!split_d) split_d = std::clamp<int64_t>(round_up(std::max<int64_t>(1, ceil_div(dec_keys, target)), 16), 128, 16384);
+  if (!split_d)
+    split_d = std::clamp<int64_t>(round_up(std::max<int64_t>(1, ceil_div(dec_keys, target)), 16),
+                                  128, DLFP_MAX_DECODE_UNIT_KEYS);
   int64_t split_p = tn.prefill_split_tokens;
-  if (!split_p) split_p = std::max<int64_t>(1024, round_up(std::max<int64_t>(1, ceil_div(pre_keys, std::max<int64_t>(1, target / 4))), 64));
+  if (!split_p)
+    split_p = std::clamp<int64_t>(
+        round_up(std::max<int64_t>(1, ceil_div(pre_keys, std::max<int64_t>(1, target / 4))), 64),
+        1024, DLFP_MAX_PREFILL_UNIT_KEYS);
 
   // Build units: prefill (KV-head-major), then decode.
   std::vector<Unit> units;
@@ -167,14 +179,14 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
       if (grp < 0 || seen[grp] >= 0) continue;
       seen[grp] = off;
       group_off[grp] = off;
-      off += (int64_t)u.f[DLFP_W_NSPLITS] * group_rows[grp] * (DLFP_HEAD_DIM + 2);
+      off += (int64_t)u.f[DLFP_W_NSPLITS] * slot_floats(group_rows[grp]);
     }
   }
   if (off > std::numeric_limits<int32_t>::max()) return DLFP_ERANGE;
   for (Unit& u : units) {
     const int32_t grp = u.f[DLFP_W_GROUP];
     if (grp < 0) continue;
-    const int64_t slot = group_rows[grp] * (DLFP_HEAD_DIM + 2);
+    const int64_t slot = slot_floats(group_rows[grp]);
     u.f[DLFP_W_WSGROUP] = (int32_t)group_off[grp];
     u.f[DLFP_W_WSOFF] = (int32_t)(group_off[grp] + u.f[DLFP_W_SPLIT] * slot);
   }

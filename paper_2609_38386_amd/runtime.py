@@ -137,7 +137,7 @@ class Iteration:
         for i in idx:   # one sequence at a time keeps each history batch small
             s = self.seqs[i]
             hist = Batch(self.dims, [s.pos0], [s.pos0], self.block_table[i:i + 1],
-                         self.pool.num_blocks, self.device, _d.dlfp_tuning(0, 1 << 20, 0))
+                         self.pool.num_blocks, self.device)
             hist.append(self.pool, bits_to_device(s.stream.k[:s.pos0], self.device),
                         bits_to_device(s.stream.v[:s.pos0], self.device))
 
@@ -150,3 +150,51 @@ class Iteration:
                               dtype=out_dtype, device=self.device)
         self.batch.attention(self.pool, self.q, scale, out, workspace)
         return out
+
+
+class StagedBatch:
+    """Per-iteration metadata with persistent buffers: the C builder fills host
+    arrays, which are packed into one pinned buffer and copied to the device in a
+    single stream-ordered transfer.  Reuse requires the previous iteration's copy
+    to have completed (callers synchronise on iteration completion anyway)."""
+
+    def __init__(self, dims: _d.dlfp_dims, cap_seqs: int, cap_tokens: int, cap_work: int, device,
+                 tuning: Optional[_d.dlfp_tuning] = None):
+        import ctypes
+        self._ct = ctypes
+        self.dims = dims
+        self.tuning = tuning if tuning is not None else _d.dlfp_tuning(0, 0, 0)
+        self.meta = _d.Meta(cap_seqs, cap_tokens, cap_work)
+        total = (cap_seqs + 1) + 2 * cap_seqs + cap_tokens + cap_work * _d.WORK_INTS
+        self.host = torch.empty(total, dtype=torch.int32, pin_memory=True)
+        self.host_np = self.host.numpy()
+        self.dev = torch.empty(total, dtype=torch.int32, device=device)
+        self.lib = _d.lib()
+
+    def build(self, q_len: np.ndarray, kv_len: np.ndarray, block_table: np.ndarray,
+              num_blocks: int, stream=None):
+        ct = self._ct
+        m = self.meta
+        st = self.lib.dlfp_build_varlen_meta(
+            ct.byref(self.dims), ct.byref(self.tuning), len(q_len), _d._ptr32(q_len),
+            _d._ptr32(kv_len), _d._ptr32(block_table), block_table.shape[1], int(num_blocks),
+            ct.byref(m.c))
+        _d._check(st, "dlfp_build_varlen_meta")
+        n, T, U = m.c.num_seqs, m.c.num_tokens, m.c.num_units
+        h = self.host_np
+        o = 0
+        offs = []
+        for arr, cnt in ((m.cu_q, n + 1), (kv_len, n), (m.q_pos0, n), (m.slot_mapping, T),
+                         (m.work_buf.reshape(-1), U * _d.WORK_INTS)):
+            h[o:o + cnt] = arr[:cnt]
+            offs.append((o, cnt))
+            o += cnt
+        self.dev[:o].copy_(self.host[:o], non_blocking=True)
+        (a, na), (b, nb), (c, nc), (d, nd), (e, ne) = offs
+        self.d_cu_q = self.dev[a:a + na]
+        self.d_kv_len = self.dev[b:b + nb]
+        self.d_q_pos0 = self.dev[c:c + nc]
+        self.d_slots = self.dev[d:d + nd]
+        self.d_work = self.dev[e:e + ne]
+        self.num_tokens = T
+        return self

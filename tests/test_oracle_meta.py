@@ -51,7 +51,7 @@ def _valid_list():
     """seq 0: prompt chunk of 70 tokens at offset 30 (kv 100), g=2 -> 64 tokens per tile;
     seq 1: decoder with kv 40 split into [0,32) and [32,40).  One KV head."""
     g, rows_t = 2, 64
-    slot = lambda rows: rows * (128 + 2)
+    slot = lambda rows: (rows * (128 + 2) + 63) // 64 * 64
     base = (256 + 4 * 65536) // 4  # header + fixed counter region, in floats
     units = [
         _unit(0, 0, 0, 64, 0, 48, grp=0, split=0, nsp=2, wsoff=base, wsgrp=base),
