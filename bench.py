@@ -45,6 +45,9 @@ def parse_args():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--quiet", action="store_true")
+    ap.add_argument("--pmc-workload", choices=["sweep", "shares"], default=None,
+                    help="counter-pass workloads: 'sweep' = one headline sweep plus a 1 GiB "
+                         "device copy; 'shares' = decode-only and prefill-only launches")
     return ap.parse_args()
 
 
@@ -385,6 +388,36 @@ def cpu_baseline(seconds):
 
 # ----------------------------------------------------------------------------- main
 
+def pmc_workload(dev, kind):
+    """'sweep': one untimed headline sweep, then a plain 1 GiB device-to-device copy
+    whose known traffic calibrates the FETCH_SIZE / WRITE_SIZE counters.
+    'shares': decode-only launches (28 layers), then prefill-only launches of the
+    last 2048-token chunk (28 layers), Qwen3-0.6B shapes."""
+    import torch
+    from paper_2609_38386_amd import workload as wl
+    cfg = wl.qwen3_0_6b_config()
+    sw = Sweep(cfg, dev, n_pools=cfg.layers, layers=cfg.layers)
+    if kind == "shares":
+        sw.iteration(cfg.chunks[0], 0, prefill=False, record=False)
+        sw.iteration(2048, cfg.prompt_len // 2048 - 1, decoders=False, record=False)
+        print(json.dumps({"decode_launches": cfg.layers, "prefill_launches": cfg.layers}))
+        return
+    n = 0
+    for p in cfg.chunks:
+        for c in sw.chunks(p, "all"):
+            sw.iteration(p, c, record=False)
+            n += 1
+    del sw
+    torch.cuda.empty_cache()
+    a = torch.empty(1 << 30, dtype=torch.uint8, device=dev).fill_(1)
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"iterations": n, "attention_launches": n * cfg.layers,
+                      "copy_bytes_each_way": 1 << 30}), flush=True)
+
+
 def main():
     args = parse_args()
     if args.gpus != 1:
@@ -399,6 +432,9 @@ def main():
         print("bench.py needs a HIP device", file=sys.stderr)
         sys.exit(1)
     dev = torch.device("cuda:0")
+    if args.pmc_workload:
+        pmc_workload(dev, args.pmc_workload)
+        return
     logf = lambda *a: log(args, *a)  # noqa: E731
     cfg, r = run_headline(args, dev, logf)
     logf(f"headline done: {r['wall']:.2f}s for {args.steps} steps")

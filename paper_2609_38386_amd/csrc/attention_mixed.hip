@@ -37,6 +37,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <type_traits>
 
 #include "dlfp.h"
 #include "dlfp_internal.h"
@@ -273,6 +274,7 @@ __device__ __forceinline__ void load_stage(Stage& st, const Args& a, const int32
 // K tile in LDS: row R (key) is 256 bytes; 16-byte chunk x sits at x ^ (R & 15).
 // V^T tile: page pg at 16 KiB + pg * 4 KiB, dim d row of 32 bytes; 8-byte slot
 // s (keys 4s..4s+3) sits at s ^ ((d >> 2) & 3).
+template <bool TAIL>  // TAIL: the stage reaches past the unit's last key
 __device__ __forceinline__ void store_stage(const Stage& st, char* buf, int tid, int k0, int ke) {
 #pragma unroll
   for (int pg = 0; pg < 4; ++pg) {
@@ -284,8 +286,10 @@ __device__ __forceinline__ void store_stage(const Stage& st, char* buf, int tid,
   for (int pg = 0; pg < 4; ++pg) {
     const int d = tid >> 1, half = tid & 1;
     u32x4_t v = st.c[4 + pg];
-    const int key0 = k0 + pg * PAGE + 8 * half;
-    if (key0 + 8 > ke) v = mask_keys(v, key0, ke);
+    if constexpr (TAIL) {
+      const int key0 = k0 + pg * PAGE + 8 * half;
+      if (key0 + 8 > ke) v = mask_keys(v, key0, ke);
+    }
     const int f = (d >> 2) & 3;
     char* rowp = buf + KV_TILE * D * 2 + pg * PAGE_ELEMS * 2 + d * 32;
     u32x2_t lo = {v[0], v[1]}, hi = {v[2], v[3]};
@@ -338,88 +342,105 @@ __device__ void prefill_unit(const Args& a, const int32_t* it, char* smem, int* 
   __syncthreads();
   Stage st;
   load_stage(st, a, ptab, kh, kb, kb, ke, tid);
-  store_stage(st, smem, tid, kb, ke);
+  if (kb + KV_TILE > ke)
+    store_stage<true>(st, smem, tid, kb, ke);
+  else
+    store_stage<false>(st, smem, tid, kb, ke);
   __syncthreads();
+
+  // One 64-key tile.  Scores stay unscaled: the running max is tracked on raw
+  // scores (the scale is positive) and the scale is folded into the exponent,
+  // p = exp2(s * c - m * c), one fma per score.  MASKED tiles (the causal
+  // diagonal and the unit's tail) compare every key with the row's limit; all
+  // other tiles skip that work.
+  auto tile = [&](const char* buf, int k0, auto masked) {
+    constexpr bool MASKED = decltype(masked)::value;
+    // S^T = K Q^T for keys [k0, k0 + 64): two 32-key blocks whose accumulators
+    // are advanced alternately so that consecutive MFMAs are independent.
+    f32x16_t sacc[2] = {f32x16_t{}, f32x16_t{}};
+#pragma unroll
+    for (int kk = 0; kk < 8; ++kk)
+#pragma unroll
+      for (int kb2 = 0; kb2 < 2; ++kb2) {
+        const int R = kb2 * 32 + col;
+        const int x = 2 * kk + hi;
+        const bf16x8_t af =
+            *reinterpret_cast<const bf16x8_t*>(buf + R * 256 + ((x ^ (R & 15)) << 4));
+        sacc[kb2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, qf[kk], sacc[kb2], 0, 0, 0);
+      }
+    // sacc[kb2][rr] holds key 32 kb2 + 8 (rr / 4) + 4 hi + rr % 4 of this lane's row.
+    float mx = -__builtin_inff();
+#pragma unroll
+    for (int kb2 = 0; kb2 < 2; ++kb2)
+#pragma unroll
+      for (int rr = 0; rr < 16; ++rr) {
+        if constexpr (MASKED) {
+          const int key = k0 + kb2 * 32 + 8 * (rr >> 2) + 4 * hi + (rr & 3);
+          sacc[kb2][rr] = key < lim ? sacc[kb2][rr] : -__builtin_inff();
+        }
+        mx = fmaxf(mx, sacc[kb2][rr]);
+      }
+    mx = fmaxf(mx, shfl_xor(mx, 32));
+    const float c = a.scale_log2;
+    const float m_new = fmaxf(m_run, mx * c);   // scaled units
+    const float alpha = fexp2(m_run - m_new);
+    m_run = m_new;
+    float psum = 0.f;
+    bf16x8_t pf[4];
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      u32x4_t pk;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const float p0 = fexp2(__builtin_fmaf(sacc[kk >> 1][8 * (kk & 1) + 2 * w], c, -m_new));
+        const float p1 = fexp2(__builtin_fmaf(sacc[kk >> 1][8 * (kk & 1) + 2 * w + 1], c, -m_new));
+        psum += p0 + p1;
+        pk[w] = pack_bf16(p0, p1);
+      }
+      pf[kk] = __builtin_bit_cast(bf16x8_t, pk);
+    }
+    l_run = l_run * alpha + psum;
+    if (__builtin_amdgcn_ballot_w64(alpha != 1.f)) {
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb) o[mb] *= alpha;
+    }
+    // O^T += V^T P^T, one 16-key page per k-step.
+    const char* vbuf = buf + KV_TILE * D * 2;
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      const char* vp = vbuf + kk * PAGE_ELEMS * 2;
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb) {
+        const int d = mb * 32 + col;
+        const int f = (d >> 2) & 3;
+        const u32x2_t lo = *reinterpret_cast<const u32x2_t*>(vp + d * 32 + ((hi ^ f) << 3));
+        const u32x2_t hv =
+            *reinterpret_cast<const u32x2_t*>(vp + d * 32 + (((2 + hi) ^ f) << 3));
+        const u32x4_t av = {lo[0], lo[1], hv[0], hv[1]};
+        o[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, av),
+                                                        pf[kk], o[mb], 0, 0, 0);
+      }
+    }
+  };
 
   for (int ti = 0; ti < ntiles; ++ti) {
     const int k0 = kb + ti * KV_TILE;
     const bool more = ti + 1 < ntiles;
     if (more) load_stage(st, a, ptab, kh, kb, k0 + KV_TILE, ke, tid);
     const char* buf = smem + (ti & 1) * STAGE_BYTES;
-
     if (wave_active) {
-      // S^T = K Q^T for keys [k0, k0 + 64): two 32-key blocks.
-      f32x16_t sacc[2];
-#pragma unroll
-      for (int kb2 = 0; kb2 < 2; ++kb2) {
-        sacc[kb2] = f32x16_t{};
-        const int R = kb2 * 32 + col;
-#pragma unroll
-        for (int kk = 0; kk < 8; ++kk) {
-          const int x = 2 * kk + hi;
-          const bf16x8_t af =
-              *reinterpret_cast<const bf16x8_t*>(buf + R * 256 + ((x ^ (R & 15)) << 4));
-          sacc[kb2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, qf[kk], sacc[kb2], 0, 0, 0);
-        }
-      }
-      // Scale, mask, running max.  sacc[kb2][rr] holds key
-      // 32 kb2 + 8 (rr / 4) + 4 hi + rr % 4 of this lane's row.
-      const bool need_mask = k0 + KV_TILE > wave_lim_min;
-      float mx = NEG_BIG;
-#pragma unroll
-      for (int kb2 = 0; kb2 < 2; ++kb2)
-#pragma unroll
-        for (int rr = 0; rr < 16; ++rr) {
-          float x = sacc[kb2][rr] * a.scale_log2;
-          if (need_mask) {
-            const int key = k0 + kb2 * 32 + 8 * (rr >> 2) + 4 * hi + (rr & 3);
-            x = key < lim ? x : -__builtin_inff();
-          }
-          sacc[kb2][rr] = x;
-          mx = fmaxf(mx, x);
-        }
-      mx = fmaxf(mx, shfl_xor(mx, 32));
-      const float m_new = fmaxf(m_run, mx);
-      const float alpha = fexp2(m_run - m_new);
-      m_run = m_new;
-      float psum = 0.f;
-      bf16x8_t pf[4];
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {
-        u32x4_t pk;
-#pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          const float p0 = fexp2(sacc[kk >> 1][8 * (kk & 1) + 2 * w] - m_new);
-          const float p1 = fexp2(sacc[kk >> 1][8 * (kk & 1) + 2 * w + 1] - m_new);
-          psum += p0 + p1;
-          pk[w] = pack_bf16(p0, p1);
-        }
-        pf[kk] = __builtin_bit_cast(bf16x8_t, pk);
-      }
-      l_run = l_run * alpha + psum;
-      if (__builtin_amdgcn_ballot_w64(alpha != 1.f)) {
-#pragma unroll
-        for (int mb = 0; mb < 4; ++mb) o[mb] *= alpha;
-      }
-      // O^T += V^T P^T, one 16-key page per k-step.
-      const char* vbuf = buf + KV_TILE * D * 2;
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {
-        const char* vp = vbuf + kk * PAGE_ELEMS * 2;
-#pragma unroll
-        for (int mb = 0; mb < 4; ++mb) {
-          const int d = mb * 32 + col;
-          const int f = (d >> 2) & 3;
-          const u32x2_t lo = *reinterpret_cast<const u32x2_t*>(vp + d * 32 + ((hi ^ f) << 3));
-          const u32x2_t hv =
-              *reinterpret_cast<const u32x2_t*>(vp + d * 32 + (((2 + hi) ^ f) << 3));
-          const u32x4_t av = {lo[0], lo[1], hv[0], hv[1]};
-          o[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, av),
-                                                          pf[kk], o[mb], 0, 0, 0);
-        }
-      }
+      if (k0 + KV_TILE > wave_lim_min)
+        tile(buf, k0, std::true_type{});
+      else
+        tile(buf, k0, std::false_type{});
     }
-    if (more) store_stage(st, smem + ((ti + 1) & 1) * STAGE_BYTES, tid, k0 + KV_TILE, ke);
+    if (more) {
+      char* nbuf = smem + ((ti + 1) & 1) * STAGE_BYTES;
+      if (k0 + 2 * KV_TILE > ke)
+        store_stage<true>(st, nbuf, tid, k0 + KV_TILE, ke);
+      else
+        store_stage<false>(st, nbuf, tid, k0 + KV_TILE, ke);
+    }
     __syncthreads();
   }
 
