@@ -1,0 +1,28 @@
+"""Replay on the device: the scheduler drives the real append + single attention launch
+and the controller reads HIP-event completion times.  Latencies are parity unpinned
+(they depend on the GPU); reconciliation and the controller's guard are checked."""
+import pytest
+import torch
+
+from paper_2609_38386_amd import replay as rp
+
+pytestmark = pytest.mark.gpu
+
+
+def test_gpu_replay_uncapped_and_dlfp():
+    assert torch.cuda.is_available()
+    dev = torch.device("cuda:0")
+    cfg = rp.ReplayConfig(seed=802, n_requests=12, rate_per_s=400.0, prompt_hi=2048, out_len=24)
+    ex = rp.GpuExecutor(cfg, dev)
+    trace = []
+    base = rp.run_replay(cfg, rp.Policy(rp.Policy.UNCAPPED), ex, trace=trace)
+    assert base["reconciled"]
+    dec_only = sorted(it["layer_ms"] for it in trace if it["decoders"] > 0 and it["p_t"] == 0)
+    assert dec_only and all(0.0 < x < 50.0 for x in dec_only)
+    target = 1.2 * dec_only[len(dec_only) // 2]
+    trace2 = []
+    dl = rp.run_replay(cfg, rp.Policy(rp.Policy.DLFP, target_ms=target, cfg=cfg), ex,
+                       trace=trace2)
+    assert dl["reconciled"]
+    assert all(it["limit"] == cfg.budget for it in trace2 if it["decoders"] == 0)
+    assert dl["guarded_iterations"] > 0
