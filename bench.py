@@ -466,9 +466,9 @@ def pmc_workload(dev, kind):
 def main():
     args = parse_args()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported by this build "
-              "(the hot path shards by KV head or by sequence with no exchange inside "
-              "attention, but no multi-GPU path is built)", file=sys.stderr)
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported: the library "
+              "has no multi-GPU path (the hot path would shard by KV head or by sequence "
+              "with no exchange inside attention)", file=sys.stderr)
         sys.exit(2)
     import torch
     from paper_2609_38386_amd import dlfp as D

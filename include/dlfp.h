@@ -90,15 +90,23 @@ typedef struct {
 } dlfp_dims;
 
 /* How the attention launch splits key ranges (split-K).  Zero fields pick
- * the built-in policy, which sizes splits so the launch has about
- * target_units units of work. */
+ * the built-in policy: prefill key ranges are cut so the prefill share offers
+ * about one unit per resident workgroup (never below 1024 keys), decode
+ * ranges into sqrt(256 W / F) keys for W decode keys over the F resident
+ * wavefronts the prefill units leave free, and a range longer than its split
+ * is cut into equal parts. */
 typedef struct {
   int32_t decode_split_tokens;   /* keys per decode unit; 0 = auto, else a multiple of 16,
                                     at most DLFP_MAX_DECODE_UNIT_KEYS */
   int32_t prefill_split_tokens;  /* keys per prefill unit; 0 = auto, else a multiple of 64,
                                     at most DLFP_MAX_PREFILL_UNIT_KEYS */
-  int32_t target_units;          /* auto policy target; 0 = 4096 */
+  int32_t target_units;          /* wavefronts the device keeps resident for the attention
+                                    launch, which the automatic split sizes are fitted to;
+                                    0 = DLFP_DEFAULT_RESIDENT_WAVES */
 } dlfp_tuning;
+
+/* 256 compute units x 8 resident wavefronts (two 256-thread workgroups per CU). */
+#define DLFP_DEFAULT_RESIDENT_WAVES 2048
 
 /* Host-side metadata of one packed batch.  The caller provides the arrays and
  * their capacities; dlfp_build_varlen_meta fills arrays and counts. */
@@ -235,6 +243,15 @@ int dlfp_timer_start(dlfp_timer timer, hipStream_t stream);
 int dlfp_timer_stop(dlfp_timer timer, hipStream_t stream);
 /* Block until the stop event has completed; elapsed device time in ms. */
 int dlfp_timer_elapsed_ms(dlfp_timer timer, double* ms);
+
+/* Enqueue on `stream` a one-wave kernel that idles for `microseconds` of
+ * device wall-clock time (1..DLFP_MAX_HOLD_US; DLFP_EINVAL otherwise).  Call
+ * it before dlfp_timer_start when the host enqueues an iteration's launches
+ * one by one: they then run back to back and the timer sees device time only,
+ * which is how one layer's share of an iteration's latency is measured.  The
+ * kernel reads the wall clock and touches no memory; it always terminates. */
+#define DLFP_MAX_HOLD_US 10000
+int dlfp_stream_hold(int32_t microseconds, hipStream_t stream);
 
 const char* dlfp_status_string(int status);
 

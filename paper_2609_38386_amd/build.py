@@ -18,7 +18,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB_PATH = os.path.join(HERE, "libdlfp.so")
 ARCH = "gfx950"
 
-SOURCES = ["dlfp_host.cpp", "kv_append.hip", "attention_mixed.hip"]
+SOURCES = ["dlfp_host.cpp", "kv_append.hip", "attention_mixed.hip", "stream_hold.hip"]
 
 # Packed FP32 instructions are kept out of device code.
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
@@ -40,7 +40,7 @@ def build_library(verbose: bool = False, jobs: int = 3) -> str:
         objs, procs = [], []
         for src in SOURCES:
             obj = os.path.join(tmp, src + ".o")
-            lang = ["-x", "hip"] if src.endswith(".hip") else ["-x", "hip"]
+            lang = ["-x", "hip"]
             cmd = [hipcc, *COMMON, *DEVICE_FLAGS, *lang, "-c", os.path.join(CSRC, src), "-o", obj]
             if verbose:
                 print(" ".join(cmd), flush=True)

@@ -486,27 +486,43 @@ __device__ void prefill_unit(const Args& a, const int32_t* it, char* smem, int* 
   __syncthreads();
   if (!*flag) return;
 
-  // Last arriver: merge every split of the group in split order.  Four
-  // threads per row, 32 dims each, two passes over the rows; the loads of a
-  // split are independent of each other.
+  // Last arriver: merge every split of the group in split order with an
+  // online rescale.  Four threads per row, 32 dims each, two passes over the
+  // rows; the loads of four splits are issued before any is consumed, so a
+  // pass costs about one memory round trip per four splits.
   for (int row = tid >> 2; row < rows; row += THREADS / 4) {
     const int quarter = tid & 3;
-    float mmax = NEG_BIG;
-    for (int j = 0; j < nsplits; ++j)
-      mmax = fmaxf(mmax, pload1(sl, j * slot_floats + rows * D + row));
-    float lsum = 0.f;
+    float M = NEG_BIG, lsum = 0.f;
     f32x4_t acc[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) acc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    for (int j = 0; j < nsplits; ++j) {
-      const int base = j * slot_floats;
-      const float w = fexp2(pload1(sl, base + rows * D + row) - mmax);
-      lsum += w * pload1(sl, base + rows * D + rows + row);
-      f32x4_t t[8];
+    for (int j = 0; j < nsplits; j += 4) {
+      float mj[4], lj[4];
+      f32x4_t x[4][8];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) t[i] = pload4(sl, base + row * D + quarter * 32 + 4 * i);
+      for (int u = 0; u < 4; ++u) {
+        const int b = min(j + u, nsplits - 1) * slot_floats;
+        mj[u] = pload1(sl, b + rows * D + row);
+        lj[u] = pload1(sl, b + rows * D + rows + row);
 #pragma unroll
-      for (int i = 0; i < 8; ++i) acc[i] += w * t[i];
+        for (int i = 0; i < 8; ++i) x[u][i] = pload4(sl, b + row * D + quarter * 32 + 4 * i);
+      }
+      float mn = M;
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (j + u < nsplits) mn = fmaxf(mn, mj[u]);
+      const float r = fexp2(M - mn);
+      M = mn;
+      lsum *= r;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) acc[i] *= r;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const float w = j + u < nsplits ? fexp2(mj[u] - mn) : 0.f;
+        lsum += w * lj[u];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[i] += w * x[u][i];
+      }
     }
     const float inv = 1.f / lsum;
     const int trow = row / G, hrow = row % G;
@@ -737,44 +753,57 @@ __device__ void decode_unit(const Args& a, const int32_t* it, char* wl) {
   old = __shfl(old, 0);
   if (old != nsplits - 1) return;
 
-  // Last arriver: lane j holds split j's statistics (64 splits at a time);
-  // weights reach the accumulating lanes by readlane, in split order.
-#pragma unroll 1
+  // Last arriver.  Entry f = j G + h stands for head h of split j.  Lanes
+  // first load the entries' maxima (64 at a time) and reduce them per head
+  // (lane l keeps the maximum of head l % G), then load the entries' row sums
+  // and weights, and accumulate the partial outputs in split order, sixteen
+  // entries' loads issued together.
+  const int nf = nsplits * G;
+  float mlane = NEG_BIG;
+  for (int f0 = 0; f0 < nf; f0 += 64) {
+    const int f = f0 + lane;
+    if (f < nf) mlane = fmaxf(mlane, pload1(sl, (f / G) * slot_floats + G * D + f % G));
+  }
+#pragma unroll
+  for (int sh = G; sh < 64; sh <<= 1) mlane = fmaxf(mlane, shfl_xor(mlane, sh));
+  float lsum[G], acc0[G], acc1[G];
+#pragma unroll
+  for (int h = 0; h < G; ++h) lsum[h] = acc0[h] = acc1[h] = 0.f;
+  for (int f0 = 0; f0 < nf; f0 += 64) {
+    const int f = f0 + lane;
+    float wf = 0.f, lf = 0.f;
+    if (f < nf) {
+      const int base = (f / G) * slot_floats + G * D;
+      wf = fexp2(pload1(sl, base + f % G) - mlane);
+      lf = pload1(sl, base + G + f % G);
+    }
+    const int n = min(64, nf - f0);
+    for (int e0 = 0; e0 < n; e0 += 16) {
+      f32x2_t v[16];
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int fe = f0 + min(e0 + e, n - 1);
+        v[e] = pload2(sl, (fe / G) * slot_floats + (fe % G) * D + 2 * lane);
+      }
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int src = min(e0 + e, n - 1);
+        const bool ok = e0 + e < n;
+        const float w = ok ? __builtin_bit_cast(float, __builtin_amdgcn_readlane(
+                                                           __builtin_bit_cast(int, wf), src))
+                           : 0.f;
+        const float lw = __builtin_bit_cast(
+            float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, lf), src));
+        lsum[e % G] += w * lw;
+        acc0[e % G] += w * v[e][0];
+        acc1[e % G] += w * v[e][1];
+      }
+    }
+  }
+#pragma unroll
   for (int h = 0; h < G; ++h) {
-    float mmax = NEG_BIG;
-    for (int j0 = 0; j0 < nsplits; j0 += 64) {
-      const int j = j0 + lane;
-      float mj = j < nsplits ? pload1(sl, j * slot_floats + G * D + h) : NEG_BIG;
-      mj = fmaxf(mj, shfl_xor(mj, 1));
-      mj = fmaxf(mj, shfl_xor(mj, 2));
-      mj = fmaxf(mj, shfl_xor(mj, 4));
-      mj = fmaxf(mj, shfl_xor(mj, 8));
-      mj = fmaxf(mj, shfl_xor(mj, 16));
-      mj = fmaxf(mj, shfl_xor(mj, 32));
-      mmax = fmaxf(mmax, mj);
-    }
-    float lsum = 0.f, acc0 = 0.f, acc1 = 0.f;
-    for (int j0 = 0; j0 < nsplits; j0 += 64) {
-      const int j = j0 + lane;
-      float wj = 0.f, lj = 0.f;
-      if (j < nsplits) {
-        wj = fexp2(pload1(sl, j * slot_floats + G * D + h) - mmax);
-        lj = pload1(sl, j * slot_floats + G * D + G + h);
-      }
-      const int n = min(64, nsplits - j0);
-      for (int jj = 0; jj < n; ++jj) {
-        const float w = __builtin_bit_cast(float, __builtin_amdgcn_readlane(
-                                                      __builtin_bit_cast(int, wj), jj));
-        const float lw = __builtin_bit_cast(float, __builtin_amdgcn_readlane(
-                                                       __builtin_bit_cast(int, lj), jj));
-        const f32x2_t v = pload2(sl, (j0 + jj) * slot_floats + h * D + 2 * lane);
-        lsum += w * lw;
-        acc0 += w * v[0];
-        acc1 += w * v[1];
-      }
-    }
-    const float inv = 1.f / lsum;
-    store2(a, obase + h * D, acc0 * inv, acc1 * inv);
+    const float inv = 1.f / lsum[h];
+    store2(a, obase + h * D, acc0[h] * inv, acc1[h] * inv);
   }
   if (lane == 0)
     __hip_atomic_store(group_counter(a.ws, grp), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

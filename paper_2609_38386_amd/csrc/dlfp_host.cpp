@@ -17,6 +17,8 @@ namespace {
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
+// Prefill key ranges start on a 64-key tile.
+constexpr int64_t KV_GRANULE_PREFILL = 64;
 
 // Floats of one partial result: O[rows][128], m[rows], l[rows], padded to 256 bytes.
 int64_t slot_floats(int64_t rows) { return round_up(rows * (DLFP_HEAD_DIM + 2), 64); }
@@ -62,10 +64,12 @@ const char* dlfp_status_string(int status) {
 // Work-list policy.  Prefill rows are packed token-major into tiles of
 // DLFP_TILE_ROWS rows (DLFP_TILE_ROWS / g tokens, each with its g query heads
 // that share one KV head).  Each tile's visible key range [0, last row's
-// position] and each decoder's range [0, kv_len) is cut into splits; splits of
-// the same rows form a group that the attention launch combines in split
-// order.  Prefill units are ordered KV-head-major so that, with workgroups
-// dealt round-robin over the XCDs, units reading the same KV head share an L2.
+// position] and each decoder's range [0, kv_len) is cut into equal splits when
+// it is longer than the split size; splits of the same rows form a group that
+// the attention launch combines in split order.  Prefill units are ordered
+// KV-head-major (with workgroups dealt round-robin over the XCDs and the
+// launch giving each XCD a contiguous range, units reading the same KV head
+// share an L2), longest tile first within a head.
 int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int32_t num_seqs,
                            const int32_t* q_len, const int32_t* kv_len,
                            const int32_t* block_table, int32_t max_blocks, int32_t num_blocks,
@@ -85,12 +89,12 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
       tn.prefill_split_tokens > DLFP_MAX_PREFILL_UNIT_KEYS)
     return DLFP_EINVAL;
   if (tn.target_units < 0) return DLFP_EINVAL;
-  const int64_t target = tn.target_units ? tn.target_units : 4096;
+  const int64_t resident = tn.target_units ? tn.target_units : DLFP_DEFAULT_RESIDENT_WAVES;
   const int hkv = dims->num_kv_heads;
   const int tile_tokens = DLFP_TILE_ROWS / g;
 
   // Validate sequences and the pages they use.
-  int64_t tokens = 0, dec_keys = 0, pre_keys = 0;
+  int64_t tokens = 0, pre_keys = 0;
   for (int s = 0; s < num_seqs; ++s) {
     const int32_t ql = q_len[s], kl = kv_len[s];
     if (ql < 1 || kl < ql) return DLFP_EINVAL;
@@ -102,9 +106,7 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
     if ((int64_t)num_blocks * DLFP_PAGE_SIZE > std::numeric_limits<int32_t>::max())
       return DLFP_ERANGE;
     tokens += ql;
-    if (ql == 1) {
-      dec_keys += (int64_t)kl * hkv;
-    } else {
+    if (ql > 1) {
       const int64_t pos0 = kl - ql;
       for (int64_t t0 = 0; t0 < ql; t0 += tile_tokens) {
         const int64_t nt = std::min<int64_t>(tile_tokens, ql - t0);
@@ -114,23 +116,51 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
   }
   if (tokens > std::numeric_limits<int32_t>::max()) return DLFP_ERANGE;
 
-  // Split sizes.
-  int64_t split_d = tn.decode_split_tokens;
-  if (!split_d)
-    split_d = std::clamp<int64_t>(round_up(std::max<int64_t>(1, ceil_div(dec_keys, target)), 16),
-                                  128, DLFP_MAX_DECODE_UNIT_KEYS);
+  // Prefill split: long key ranges are cut so that the prefill share offers
+  // about one unit per resident workgroup (four wavefronts), never below 1024
+  // keys.
   int64_t split_p = tn.prefill_split_tokens;
   if (!split_p)
     split_p = std::clamp<int64_t>(
-        round_up(std::max<int64_t>(1, ceil_div(pre_keys, std::max<int64_t>(1, target / 4))), 64),
+        round_up(std::max<int64_t>(1, ceil_div(pre_keys, std::max<int64_t>(1, resident / 4))), 64),
         1024, DLFP_MAX_PREFILL_UNIT_KEYS);
+  // Decode split.  The launch time is roughly the share of work per resident
+  // wavefront plus the longest unit, and every unit adds a fixed cost (query
+  // and block-table loads, pipeline fill, its part of the merge) worth about
+  // 256 keys; the split minimising the sum is sqrt(256 W / F) keys for W
+  // decode keys over the F wavefronts the prefill units leave free (a prefill
+  // workgroup holds four; at least half stay free).
+  int64_t split_d = tn.decode_split_tokens;
+  if (!split_d) {
+    int64_t pre_units = 0, dec_keys = 0;
+    for (int s = 0; s < num_seqs; ++s) {
+      if (q_len[s] == 1) {
+        dec_keys += (int64_t)kv_len[s] * hkv;
+        continue;
+      }
+      const int64_t pos0 = kv_len[s] - q_len[s];
+      for (int64_t t0 = 0; t0 < q_len[s]; t0 += tile_tokens) {
+        const int64_t nt = std::min<int64_t>(tile_tokens, q_len[s] - t0);
+        pre_units += hkv * ceil_div(pos0 + t0 + nt, split_p);
+      }
+    }
+    const int64_t free_waves = resident - 4 * std::min(pre_units, resident / 8);
+    const double best = std::sqrt(256.0 * (double)dec_keys / (double)std::max<int64_t>(1, free_waves));
+    split_d = std::clamp<int64_t>(round_up((int64_t)std::ceil(best), DLFP_PAGE_SIZE), 128,
+                                  DLFP_MAX_DECODE_UNIT_KEYS);
+  }
 
   // Build units: prefill (KV-head-major), then decode.
   std::vector<Unit> units;
   int32_t groups = 0;
   std::vector<int64_t> group_rows;  // rows of each group
-  auto emit = [&](int s, int kh, int64_t t0, int64_t nt, int64_t kend, int64_t split, int kind) {
-    const int64_t nsp = ceil_div(kend, split);
+  // A key range longer than the split is cut into equal parts (rounded up
+  // to the granule), so the units of a group finish together.
+  auto emit = [&](int s, int kh, int64_t t0, int64_t nt, int64_t kend, int64_t split,
+                  int64_t granule, int kind) {
+    int64_t nsp = ceil_div(kend, split);
+    const int64_t part = round_up(ceil_div(kend, nsp), granule);
+    nsp = ceil_div(kend, part);
     const int32_t grp = nsp > 1 ? groups++ : -1;
     if (nsp > 1) group_rows.push_back(nt * g);
     for (int64_t j = 0; j < nsp; ++j) {
@@ -140,8 +170,8 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
       u.f[DLFP_W_KVHEAD] = kh;
       u.f[DLFP_W_QTOK0] = (int32_t)t0;
       u.f[DLFP_W_QNTOK] = (int32_t)nt;
-      u.f[DLFP_W_KVBEGIN] = (int32_t)(j * split);
-      u.f[DLFP_W_KVEND] = (int32_t)std::min(kend, (j + 1) * split);
+      u.f[DLFP_W_KVBEGIN] = (int32_t)(j * part);
+      u.f[DLFP_W_KVEND] = (int32_t)std::min(kend, (j + 1) * part);
       u.f[DLFP_W_GROUP] = grp;
       u.f[DLFP_W_SPLIT] = (int32_t)j;
       u.f[DLFP_W_NSPLITS] = (int32_t)nsp;
@@ -149,19 +179,34 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
       units.push_back(u);
     }
   };
-  for (int kh = 0; kh < hkv; ++kh)
+  // Prefill tiles of one KV head go longest first, so that the workgroups of
+  // an XCD (which takes a contiguous range of prefill units) start the long
+  // tiles early.
+  struct Tile {
+    int s;
+    int64_t t0, nt, kend;
+  };
+  std::vector<Tile> tiles;
+  for (int kh = 0; kh < hkv; ++kh) {
+    tiles.clear();
     for (int s = 0; s < num_seqs; ++s) {
       if (q_len[s] == 1) continue;
       const int64_t pos0 = kv_len[s] - q_len[s];
       for (int64_t t0 = 0; t0 < q_len[s]; t0 += tile_tokens) {
         const int64_t nt = std::min<int64_t>(tile_tokens, q_len[s] - t0);
-        emit(s, kh, t0, nt, pos0 + t0 + nt, split_p, DLFP_KIND_PREFILL);
+        tiles.push_back(Tile{s, t0, nt, pos0 + t0 + nt});
       }
     }
+    std::stable_sort(tiles.begin(), tiles.end(),
+                     [](const Tile& x, const Tile& y) { return x.kend > y.kend; });
+    for (const Tile& t : tiles)
+      emit(t.s, kh, t.t0, t.nt, t.kend, split_p, KV_GRANULE_PREFILL, DLFP_KIND_PREFILL);
+  }
   const int64_t num_prefill = (int64_t)units.size();
   for (int s = 0; s < num_seqs; ++s) {
     if (q_len[s] != 1) continue;
-    for (int kh = 0; kh < hkv; ++kh) emit(s, kh, 0, 1, kv_len[s], split_d, DLFP_KIND_DECODE);
+    for (int kh = 0; kh < hkv; ++kh)
+      emit(s, kh, 0, 1, kv_len[s], split_d, DLFP_PAGE_SIZE, DLFP_KIND_DECODE);
   }
   if ((int64_t)units.size() > std::numeric_limits<int32_t>::max() / DLFP_WORK_INTS)
     return DLFP_ERANGE;

@@ -68,7 +68,8 @@ class dlfp_controller(ctypes.Structure):
 EXPORTS = ["dlfp_build_varlen_meta", "dlfp_kv_append", "dlfp_attention_mixed",
            "dlfp_workspace_init", "dlfp_workspace_error", "dlfp_controller_init",
            "dlfp_controller_step", "dlfp_timer_create", "dlfp_timer_destroy", "dlfp_timer_start",
-           "dlfp_timer_stop", "dlfp_timer_elapsed_ms", "dlfp_status_string", "dlfp_version"]
+           "dlfp_timer_stop", "dlfp_timer_elapsed_ms", "dlfp_stream_hold", "dlfp_status_string",
+           "dlfp_version"]
 
 
 def lib_path() -> str:
@@ -103,6 +104,7 @@ def lib():
     L.dlfp_timer_start.argtypes = [vp, vp]
     L.dlfp_timer_stop.argtypes = [vp, vp]
     L.dlfp_timer_elapsed_ms.argtypes = [vp, ctypes.POINTER(ctypes.c_double)]
+    L.dlfp_stream_hold.argtypes = [ctypes.c_int32, vp]
     L.dlfp_status_string.argtypes = [ctypes.c_int]
     L.dlfp_status_string.restype = ctypes.c_char_p
     L.dlfp_version.argtypes = []
@@ -241,6 +243,15 @@ def dlfp_controller_step(ctrl: dlfp_controller, num_decoding_next: int, last_was
                                       1 if last_was_guarded else 0, float(observed_ms),
                                       ctypes.byref(out)), "dlfp_controller_step")
     return int(out.value)
+
+
+MAX_HOLD_US = 10000
+
+
+def dlfp_stream_hold(microseconds: int, stream=None) -> None:
+    """Idle the stream for `microseconds` of device time so that launches enqueued
+    meanwhile run back to back (see dlfp.h)."""
+    _check(lib().dlfp_stream_hold(int(microseconds), _stream(stream)), "dlfp_stream_hold")
 
 
 class Timer:

@@ -289,6 +289,7 @@ class GpuExecutor:
         self.ws = rt.Workspace(device, 64 << 20)
         self.timer = D.Timer()
         self.scale = 1.0 / math.sqrt(128)
+        self.hold_us = 300
 
     def __call__(self, q_len: np.ndarray, kv_len: np.ndarray, bt: np.ndarray) -> float:
         D = self.D
@@ -299,6 +300,9 @@ class GpuExecutor:
         d_bt.view(-1).copy_(self.bt_host[:n], non_blocking=True)
         T = st.num_tokens
         ws = self.ws.ensure(st.meta.workspace_bytes)
+        # Launch marshalling happens while the stream idles, so the events bracket
+        # the layer's device work and not the host's launch gaps.
+        D.dlfp_stream_hold(self.hold_us)
         self.timer.start()
         D.dlfp_kv_append(self.dims, self.k[:T], self.v[:T], st.d_slots, self.pool.k, self.pool.v)
         D.dlfp_attention_mixed(self.dims, st.meta, st.d_cu_q, st.d_kv_len, st.d_q_pos0, st.d_work,

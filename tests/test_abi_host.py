@@ -160,3 +160,10 @@ def test_controller_rejects_bad_observation_without_state_change():
         D.dlfp_controller_init(80.0, 512, 1024, 6144)
     with pytest.raises(D.DlfpError):
         D.dlfp_controller_init(float("nan"), 3072, 1024, 6144)
+
+
+def test_stream_hold_rejects_out_of_range_durations_before_any_launch():
+    for us in (0, -5, D.MAX_HOLD_US + 1):
+        with pytest.raises(D.DlfpError) as e:
+            D.dlfp_stream_hold(us, stream=0)
+        assert e.value.status == -1
