@@ -36,7 +36,10 @@
  *  - k_new,v_new [num_tokens][Hkv][128]       this iteration's keys/values
  *  - k_cache     [num_blocks][Hkv][16][128]   key page: 16 token rows
  *  - v_cache     [num_blocks][Hkv][128][16]   value page: stored transposed,
- *                                             one 32-byte row per dimension
+ *                                             one 32-byte row per dimension;
+ *                                             slot t sits at position
+ *                                             pi(t), pi swapping slots 4-7
+ *                                             with 8-11 (bits 2 and 3 of t)
  *  - block_table [num_seqs][max_blocks] int32 physical block of each page
  *  - out         [num_tokens][Hq][128]        bf16 or fp32
  *  Token j of sequence s lives in block block_table[s][j / 16], slot j % 16;

@@ -6,7 +6,8 @@ unchanged, Sec. 3.2).  The pool layout gathered here is the one the library
 declares for its caches (16-token pages, head_dim 128, bf16):
 
 * key pages   ``k_cache[block][kv_head][slot][dim]``  (token rows)
-* value pages ``v_cache[block][kv_head][dim][slot]``  (transposed page)
+* value pages ``v_cache[block][kv_head][dim][pi(slot)]``  (transposed page;
+  ``pi`` swaps bits 2 and 3 of the slot, i.e. slots 4-7 trade places with 8-11)
 
 Token ``j`` of sequence ``s`` lives in block ``block_table[s][j // 16]`` at slot
 ``j % 16``.  Plain loops, one token at a time.
@@ -16,6 +17,12 @@ from __future__ import annotations
 import numpy as np
 
 PAGE = 16
+
+
+def value_position(slot: int) -> int:
+    """Position of token slot ``slot`` inside a value page row (bits 2 and 3 swap)."""
+    b2, b3 = (slot >> 2) & 1, (slot >> 3) & 1
+    return (slot & 3) | (b2 << 3) | (b3 << 2)
 
 
 def gather_sequence(k_cache: np.ndarray, v_cache: np.ndarray, block_row: np.ndarray,
@@ -30,7 +37,7 @@ def gather_sequence(k_cache: np.ndarray, v_cache: np.ndarray, block_row: np.ndar
         block = int(block_row[j // PAGE])
         slot = j % PAGE
         k[j] = k_cache[block, :, slot, :]
-        v[j] = v_cache[block, :, :, slot]
+        v[j] = v_cache[block, :, :, value_position(slot)]
     return k, v
 
 
@@ -43,5 +50,5 @@ def gather_slots(cache_k: np.ndarray, cache_v: np.ndarray, slots: np.ndarray):
     for i, slot in enumerate(slots):
         block, off = int(slot) // PAGE, int(slot) % PAGE
         k[i] = cache_k[block, :, off, :]
-        v[i] = cache_v[block, :, :, off]
+        v[i] = cache_v[block, :, :, value_position(off)]
     return k, v

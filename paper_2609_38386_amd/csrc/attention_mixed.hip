@@ -57,9 +57,8 @@ constexpr int PAGE = DLFP_PAGE_SIZE;
 constexpr int PAGE_ELEMS = PAGE * D;          // bf16 elements per (block, head) page
 constexpr int KV_TILE = 64;                   // keys per prefill tile (4 pages)
 constexpr int THREADS = 256;
-constexpr int STAGE_BYTES = 2 * KV_TILE * D * 2;   // K tile + V^T tile
 constexpr int PRE_PTAB = DLFP_MAX_PREFILL_UNIT_KEYS / PAGE;  // block ids of one prefill unit
-constexpr int LDS_BYTES = 2 * STAGE_BYTES + PRE_PTAB * 4;    // 64 KiB of stages + 8 KiB
+constexpr int LDS_BYTES = 4 * KV_TILE * D * 2 + PRE_PTAB * 4;  // 64 KiB of K/V tiles + 8 KiB
 constexpr int DEC_PTAB = DLFP_MAX_DECODE_UNIT_KEYS / PAGE;   // block ids of one decode unit
 // Per decode wave: K page, V page, probability buffer, block ids, and (for
 // g = 8) the query of the group.
@@ -231,71 +230,57 @@ __device__ __forceinline__ void store2(const Args& a, int64_t elem, float v0, fl
   }
 }
 
-// Keep the lanes of a 16-bit-element vector whose key index is < limit; zero the rest.
-__device__ __forceinline__ u32x4_t mask_keys(u32x4_t v, int key0, int limit) {
-  const int n = limit - key0;  // elements e < n survive
+// ---------------------------------------------------------------- prefill
+
+// Prefill LDS map: K tiles in two slots at 0 and 16 KiB, V^T tiles in two
+// slots at 32 and 48 KiB, the unit's block ids from 64 KiB.
+constexpr int TILE_BYTES = KV_TILE * D * 2;  // 16 KiB: 64 keys of K, or of V^T
+constexpr int V_BASE = 2 * TILE_BYTES;
+constexpr int PTAB_BASE = 4 * TILE_BYTES;
+// A running row maximum is only raised once a tile's maximum exceeds it by
+// more than this many powers of two, so probabilities stay below 2^8 and the
+// accumulators are rescaled rarely (the final division by the row sum makes
+// the result independent of the reference maximum).
+constexpr float RESCALE_LOG2 = 8.f;
+
+// V^T rows (dims) store their two 16-byte halves swapped when bits 2 and 3
+// of the dim differ; 8 (or 16) consecutive dims then cover every LDS bank
+// once for each half.
+__device__ __forceinline__ int vt_swz(int d) { return ((d >> 2) ^ (d >> 3)) & 1; }
+
+// Position of token slot t inside a V^T row of the cache: slots 4-7 and 8-11
+// trade places (bits 2 and 3 swap), matching the key order of the
+// S^T accumulator rows that become the PV operand.
+__device__ __forceinline__ int vt_pos(int t) { return (t & 3) | ((t & 4) << 1) | ((t & 8) >> 1); }
+
+typedef __attribute__((address_space(3))) char* lds_ptr_t;
+// One 16-byte piece per lane, global to LDS without registers: lane l's piece
+// lands at LDS byte address lds + 16 l (lds is wave-uniform).  Completion is
+// counted by the vector-memory counter; the caller waits for it explicitly
+// (wait_memory_complete) before the barrier that publishes the tile.  The
+// copy is written as assembly so that the compiler, which cannot tell the
+// ring slots apart, does not wait for it before every LDS read.
+__device__ __forceinline__ void lds_copy16(const char* src, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(src), "s"(lds)
+               : "memory", "m0");
+}
+__device__ __forceinline__ uint32_t lds_addr(char* p) {
+  return (uint32_t)(uintptr_t)(lds_ptr_t)p;
+}
+
+// Keep the elements of a 16-bit-element vector whose key index is below
+// limit; key_of(e) gives element e's key.
+template <typename F>
+__device__ __forceinline__ u32x4_t mask_elems(u32x4_t v, int limit, F key_of) {
 #pragma unroll
   for (int w = 0; w < 4; ++w) {
-    const uint32_t lo = (2 * w < n) ? 0x0000FFFFu : 0u;
-    const uint32_t hi = (2 * w + 1 < n) ? 0xFFFF0000u : 0u;
+    const uint32_t lo = key_of(2 * w) < limit ? 0x0000FFFFu : 0u;
+    const uint32_t hi = key_of(2 * w + 1) < limit ? 0xFFFF0000u : 0u;
     v[w] &= (lo | hi);
   }
   return v;
-}
-
-// ---------------------------------------------------------------- prefill
-
-// One 64-key stage: 4 pages of K and 4 pages of V^T; thread t moves 16-byte
-// chunk t of each page (a page is 256 chunks).
-struct Stage {
-  u32x4_t c[8];
-};
-
-// ptab: the unit's block ids in LDS, ptab[i] = block of page kb / 16 + i.
-__device__ __forceinline__ void load_stage(Stage& st, const Args& a, const int32_t* ptab, int kh,
-                                           int kb, int k0, int ke, int tid) {
-  // Straight-line on purpose: pages past the unit's last key re-read its last
-  // page (an L2 hit; every key there is masked), and a block id outside the
-  // pool is replaced by block 0 after raising the error word.  Block ids come
-  // from LDS, so waiting for them never waits for the tile loads in flight.
-  const int last_page = (ke - 1) / PAGE;
-#pragma unroll
-  for (int pg = 0; pg < 4; ++pg) {
-    const int page = min(k0 / PAGE + pg, last_page);
-    const int raw = ptab[page - kb / PAGE];
-    const bool ok = (unsigned)raw < (unsigned)a.num_blocks;
-    if (!ok && tid == 0) raise_error(a.ws);
-    const int64_t base = ((int64_t)(ok ? raw : 0) * a.hkv + kh) * PAGE_ELEMS + tid * 8;
-    st.c[pg] = *reinterpret_cast<const u32x4_t*>(a.kc + base);
-    st.c[4 + pg] = *reinterpret_cast<const u32x4_t*>(a.vc + base);
-  }
-}
-
-// K tile in LDS: row R (key) is 256 bytes; 16-byte chunk x sits at x ^ (R & 15).
-// V^T tile: page pg at 16 KiB + pg * 4 KiB, dim d row of 32 bytes; 8-byte slot
-// s (keys 4s..4s+3) sits at s ^ ((d >> 2) & 3).
-template <bool TAIL>  // TAIL: the stage reaches past the unit's last key
-__device__ __forceinline__ void store_stage(const Stage& st, char* buf, int tid, int k0, int ke) {
-#pragma unroll
-  for (int pg = 0; pg < 4; ++pg) {
-    const int row = tid >> 4, x = tid & 15;
-    const int R = pg * PAGE + row;
-    *reinterpret_cast<u32x4_t*>(buf + R * 256 + ((x ^ (R & 15)) << 4)) = st.c[pg];
-  }
-#pragma unroll
-  for (int pg = 0; pg < 4; ++pg) {
-    const int d = tid >> 1, half = tid & 1;
-    u32x4_t v = st.c[4 + pg];
-    if constexpr (TAIL) {
-      const int key0 = k0 + pg * PAGE + 8 * half;
-      if (key0 + 8 > ke) v = mask_keys(v, key0, ke);
-    }
-    const int f = (d >> 2) & 3;
-    char* rowp = buf + KV_TILE * D * 2 + pg * PAGE_ELEMS * 2 + d * 32;
-    u32x2_t lo = {v[0], v[1]}, hi = {v[2], v[3]};
-    *reinterpret_cast<u32x2_t*>(rowp + (((2 * half) ^ f) << 3)) = lo;
-    *reinterpret_cast<u32x2_t*>(rowp + (((2 * half + 1) ^ f) << 3)) = hi;
-  }
 }
 
 template <int G>
@@ -313,7 +298,7 @@ __device__ void prefill_unit(const Args& a, const int32_t* it, char* smem, int* 
   const int tr = r / G, hh = r % G;    // token within the unit, head within the group
   const bool row_ok = tr < nt;
   const int lim = row_ok ? min(pos0 + t0 + tr + 1, ke) : 0;  // keys < lim are visible
-  const int wave_tok0 = (wave * 32) / G;
+  const int wave_tok0 = uniform((wave * 32) / G);
   const bool wave_active = wave_tok0 < nt;
   const int wave_lim_min = min(pos0 + t0 + wave_tok0 + 1, ke);
 
@@ -326,122 +311,221 @@ __device__ void prefill_unit(const Args& a, const int32_t* it, char* smem, int* 
     for (int kk = 0; kk < 8; ++kk)
       qf[kk] = *reinterpret_cast<const bf16x8_t*>(a.q + qrow + 16 * kk + 8 * hi);
   }
-  wait_memory_complete();  // queries resident before the KV pipeline starts
+
+  const int ntiles = (ke - kb + KV_TILE - 1) / KV_TILE;
+  const int first_page = kb / PAGE, last_page = (ke - 1) / PAGE;
+  int32_t* ptab = reinterpret_cast<int32_t*>(smem + PTAB_BASE);
+  for (int i = tid; i <= last_page - first_page; i += THREADS) ptab[i] = bt[first_page + i];
+  wait_memory_complete();  // queries and block ids resident before the KV pipeline starts
+  __syncthreads();
+
+  // Copies: wave w moves page w of each 64-key tile, its 16 K rows and its
+  // 128 V^T rows, as four 1 KiB pieces each.  K row R keeps 16-byte chunk x
+  // at position x ^ (R & 15); V^T row d keeps half h at position h ^ vt_swz(d).
+  uint32_t koff[4], voff[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int rr = 4 * i + (lane >> 4);
+    koff[i] = rr * 256 + (((lane & 15) ^ rr) << 4);
+    const int d = 32 * i + (lane >> 1);
+    voff[i] = d * 32 + (((lane & 1) ^ vt_swz(d)) << 4);
+  }
+  // Straight-line on purpose: a page past the unit's last key re-reads its
+  // last page (every key there is masked), and a block id outside the pool is
+  // replaced by block 0 after raising the error word.
+  // Element offset of this wave's page of tile t (same in both caches).
+  auto page_off = [&](int t) -> int64_t {
+    const int page = min(first_page + 4 * t + wave, last_page);
+    const int raw = uniform(ptab[page - first_page]);
+    const bool ok = (unsigned)raw < (unsigned)a.num_blocks;
+    if (!ok && lane == 0) raise_error(a.ws);
+    return ((int64_t)(ok ? raw : 0) * a.hkv + kh) * PAGE_ELEMS;
+  };
+  const uint32_t lds_wave = lds_addr(smem) + uniform(wave) * (PAGE * 256);
+  auto issue_k = [&](int64_t off, int slot) {
+    const char* src = reinterpret_cast<const char*>(a.kc + off);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) lds_copy16(src + koff[i], lds_wave + slot * TILE_BYTES + i * 1024);
+  };
+  auto issue_v = [&](int64_t off, int slot) {
+    const char* src = reinterpret_cast<const char*>(a.vc + off);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      lds_copy16(src + voff[i], lds_wave + V_BASE + slot * TILE_BYTES + i * 1024);
+  };
+  // Values past the unit's last key are zeroed in LDS (a probability of 0
+  // times a NaN left in an unused slot would still be NaN).
+  auto zero_v_tail = [&](int slot, int k0) {
+    const int pg = tid >> 6;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int d = 2 * (tid & 63) + (c >> 1), h = c & 1;
+      char* p = smem + V_BASE + slot * TILE_BYTES + pg * (PAGE * 256) + d * 32 + (h << 4);
+      const int half = h ^ vt_swz(d);
+      const int key0 = k0 + pg * PAGE;
+      *reinterpret_cast<u32x4_t*>(p) = mask_elems(*reinterpret_cast<const u32x4_t*>(p), ke,
+                                                   [&](int e) { return key0 + vt_pos(8 * half + e); });
+    }
+  };
+
+  // Per-lane LDS offsets.  K: chunk (2kk + hi) of row R = 32 kb2 + col sits at
+  // ((2kk + hi) ^ (col & 15)) << 4, i.e. kbase ^ (kk << 5).  V^T: half hi of
+  // dim row d = 32 mb + col, at a lane-constant offset plus immediates.
+  const int kbase = col * 256 + ((hi ^ (col & 15)) << 4);
+  const int vbase = V_BASE + col * 32 + ((hi ^ vt_swz(col)) << 4);
 
   float m_run = NEG_BIG, l_run = 0.f;
   f32x16_t o[4];
 #pragma unroll
   for (int mb = 0; mb < 4; ++mb) o[mb] = f32x16_t{};
+  const float c = a.scale_log2;
 
-  const int ntiles = (ke - kb + KV_TILE - 1) / KV_TILE;
-  // The unit's slice of the block table goes to LDS first.
-  int32_t* ptab = reinterpret_cast<int32_t*>(smem + 2 * STAGE_BYTES);
-  const int n_pages = (ke + PAGE - 1) / PAGE - kb / PAGE;
-  for (int i = tid; i < n_pages; i += THREADS) ptab[i] = bt[kb / PAGE + i];
-  wait_memory_complete();
-  __syncthreads();
-  Stage st;
-  load_stage(st, a, ptab, kh, kb, kb, ke, tid);
-  if (kb + KV_TILE > ke)
-    store_stage<true>(st, smem, tid, kb, ke);
-  else
-    store_stage<false>(st, smem, tid, kb, ke);
-  __syncthreads();
-
-  // One 64-key tile.  Scores stay unscaled: the running max is tracked on raw
-  // scores (the scale is positive) and the scale is folded into the exponent,
-  // p = exp2(s * c - m * c), one fma per score.  MASKED tiles (the causal
-  // diagonal and the unit's tail) compare every key with the row's limit; all
-  // other tiles skip that work.
-  auto tile = [&](const char* buf, int k0, auto masked) {
-    constexpr bool MASKED = decltype(masked)::value;
-    // S^T = K Q^T for keys [k0, k0 + 64): two 32-key blocks whose accumulators
-    // are advanced alternately so that consecutive MFMAs are independent.
-    f32x16_t sacc[2] = {f32x16_t{}, f32x16_t{}};
+  // S^T = K Q^T for the 64 keys of the tile in K slot `slot`: two 32-key
+  // accumulators advanced alternately.  sacc[kb2][rr] holds key
+  // 32 kb2 + 8 (rr / 4) + 4 hi + rr % 4 of this lane's row.
+  auto qk = [&](f32x16_t* sacc, int slot) {
+    sacc[0] = f32x16_t{};
+    sacc[1] = f32x16_t{};
 #pragma unroll
-    for (int kk = 0; kk < 8; ++kk)
-#pragma unroll
-      for (int kb2 = 0; kb2 < 2; ++kb2) {
-        const int R = kb2 * 32 + col;
-        const int x = 2 * kk + hi;
-        const bf16x8_t af =
-            *reinterpret_cast<const bf16x8_t*>(buf + R * 256 + ((x ^ (R & 15)) << 4));
-        sacc[kb2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, qf[kk], sacc[kb2], 0, 0, 0);
-      }
-    // sacc[kb2][rr] holds key 32 kb2 + 8 (rr / 4) + 4 hi + rr % 4 of this lane's row.
-    float mx = -__builtin_inff();
+    for (int kk = 0; kk < 8; ++kk) {
+      const char* kp = smem + slot * TILE_BYTES + (kbase ^ (kk << 5));
+      const bf16x8_t k0f = *reinterpret_cast<const bf16x8_t*>(kp);
+      const bf16x8_t k1f = *reinterpret_cast<const bf16x8_t*>(kp + 32 * 256);
+      sacc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0f, qf[kk], sacc[0], 0, 0, 0);
+      sacc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1f, qf[kk], sacc[1], 0, 0, 0);
+    }
+  };
+  // Causal and tail mask for a tile starting at key k0 (raw scores).
+  auto mask = [&](f32x16_t* sacc, int k0) {
 #pragma unroll
     for (int kb2 = 0; kb2 < 2; ++kb2)
 #pragma unroll
       for (int rr = 0; rr < 16; ++rr) {
-        if constexpr (MASKED) {
-          const int key = k0 + kb2 * 32 + 8 * (rr >> 2) + 4 * hi + (rr & 3);
-          sacc[kb2][rr] = key < lim ? sacc[kb2][rr] : -__builtin_inff();
-        }
-        mx = fmaxf(mx, sacc[kb2][rr]);
+        const int key = k0 + kb2 * 32 + 8 * (rr >> 2) + 4 * hi + (rr & 3);
+        sacc[kb2][rr] = key < lim ? sacc[kb2][rr] : -__builtin_inff();
       }
-    mx = fmaxf(mx, shfl_xor(mx, 32));
-    const float c = a.scale_log2;
-    const float m_new = fmaxf(m_run, mx * c);   // scaled units
-    const float alpha = fexp2(m_run - m_new);
-    m_run = m_new;
-    float psum = 0.f;
-    bf16x8_t pf[4];
+  };
+  // Row maximum of a tile (raw scores), both halves of the row.
+  auto rowmax = [&](const f32x16_t* sacc) {
+    float mx = -__builtin_inff();
+#pragma unroll
+    for (int kb2 = 0; kb2 < 2; ++kb2)
+#pragma unroll
+      for (int rr = 0; rr < 16; ++rr) mx = fmaxf(mx, sacc[kb2][rr]);
+    const auto sw = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(int, mx),
+                                                     __builtin_bit_cast(int, mx), false, false);
+    return fmaxf(__builtin_bit_cast(float, sw[0]), __builtin_bit_cast(float, sw[1]));
+  };
+  // Raise the reference maximum where a tile exceeds it by more than
+  // RESCALE_LOG2 (scaled units); the accumulators follow.
+  auto rebase = [&](float mx) {
+    const float m_tile = mx * c;
+    if (__builtin_amdgcn_ballot_w64(m_tile > m_run + RESCALE_LOG2)) {
+      const float m_new = m_tile > m_run + RESCALE_LOG2 ? m_tile : m_run;
+      const float alpha = fexp2(m_run - m_new);
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb) o[mb] *= alpha;
+    }
+  };
+  // P^T = exp2(S^T c - m) rounded to bf16, as the B operands of the four
+  // 16-key steps of PV; pf[kk] holds keys 16 kk + {0-3, 8-11} + 4 hi.
+  auto probs = [&](const f32x16_t* sacc, bf16x8_t* pf) {
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
       u32x4_t pk;
 #pragma unroll
       for (int w = 0; w < 4; ++w) {
-        const float p0 = fexp2(__builtin_fmaf(sacc[kk >> 1][8 * (kk & 1) + 2 * w], c, -m_new));
-        const float p1 = fexp2(__builtin_fmaf(sacc[kk >> 1][8 * (kk & 1) + 2 * w + 1], c, -m_new));
-        psum += p0 + p1;
+        const float p0 = fexp2(__builtin_fmaf(sacc[kk >> 1][8 * (kk & 1) + 2 * w], c, -m_run));
+        const float p1 = fexp2(__builtin_fmaf(sacc[kk >> 1][8 * (kk & 1) + 2 * w + 1], c, -m_run));
         pk[w] = pack_bf16(p0, p1);
       }
       pf[kk] = __builtin_bit_cast(bf16x8_t, pk);
     }
-    l_run = l_run * alpha + psum;
-    if (__builtin_amdgcn_ballot_w64(alpha != 1.f)) {
-#pragma unroll
-      for (int mb = 0; mb < 4; ++mb) o[mb] *= alpha;
-    }
-    // O^T += V^T P^T, one 16-key page per k-step.
-    const char* vbuf = buf + KV_TILE * D * 2;
+  };
+  // Row sum of the rounded probabilities (this half of the row).
+  auto rowsum = [&](const bf16x8_t* pf) {
+    constexpr uint32_t ONES = 0x3F803F80u;  // two bf16 1.0
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
-      const char* vp = vbuf + kk * PAGE_ELEMS * 2;
+      const u32x4_t pk = __builtin_bit_cast(u32x4_t, pf[kk]);
 #pragma unroll
-      for (int mb = 0; mb < 4; ++mb) {
-        const int d = mb * 32 + col;
-        const int f = (d >> 2) & 3;
-        const u32x2_t lo = *reinterpret_cast<const u32x2_t*>(vp + d * 32 + ((hi ^ f) << 3));
-        const u32x2_t hv =
-            *reinterpret_cast<const u32x2_t*>(vp + d * 32 + (((2 + hi) ^ f) << 3));
-        const u32x4_t av = {lo[0], lo[1], hv[0], hv[1]};
-        o[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, av),
-                                                        pf[kk], o[mb], 0, 0, 0);
-      }
+      for (int w = 0; w < 4; ++w) l_run = dot2(pk[w], ONES, l_run);
     }
   };
+  // O^T += V^T P^T over the tile in V slot `slot`.
+  auto pv = [&](const bf16x8_t* pf, int slot) {
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb) {
+        const bf16x8_t vf = *reinterpret_cast<const bf16x8_t*>(
+            smem + vbase + slot * TILE_BYTES + kk * (PAGE * 256) + mb * 1024);
+        o[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[kk], o[mb], 0, 0, 0);
+      }
+  };
+  const bool tail = kb + ntiles * KV_TILE > ke;  // the last tile reaches past the unit's keys
 
-  for (int ti = 0; ti < ntiles; ++ti) {
-    const int k0 = kb + ti * KV_TILE;
-    const bool more = ti + 1 < ntiles;
-    if (more) load_stage(st, a, ptab, kh, kb, k0 + KV_TILE, ke, tid);
-    const char* buf = smem + (ti & 1) * STAGE_BYTES;
-    if (wave_active) {
-      if (k0 + KV_TILE > wave_lim_min)
-        tile(buf, k0, std::true_type{});
-      else
-        tile(buf, k0, std::false_type{});
-    }
-    if (more) {
-      char* nbuf = smem + ((ti + 1) & 1) * STAGE_BYTES;
-      if (k0 + 2 * KV_TILE > ke)
-        store_stage<true>(st, nbuf, tid, k0 + KV_TILE, ke);
-      else
-        store_stage<false>(st, nbuf, tid, k0 + KV_TILE, ke);
-    }
+  // Prologue: tiles 0 (K and V) and 1 (K) in flight, then S_0.  off_next
+  // carries the page of tile j + 1 from the step that loaded its keys to the
+  // step that loads its values.
+  int64_t off_next = page_off(0);
+  issue_k(off_next, 0);
+  issue_v(off_next, 0);
+  if (ntiles > 1) {
+    off_next = page_off(1);
+    issue_k(off_next, 1);
+  }
+  wait_memory_complete();
+  __syncthreads();
+  if (tail && ntiles == 1) {
+    zero_v_tail(0, kb);
     __syncthreads();
+  }
+  f32x16_t sa[2], sb[2];
+  if (wave_active) {
+    qk(sa, 0);
+    if (kb + KV_TILE > wave_lim_min) mask(sa, kb);
+    rebase(rowmax(sa));
+  }
+  __syncthreads();  // K slot 0 is refilled below
+
+  // Iteration j: loads of K_{j+2} and V_{j+1} go out; S_{j+1} = K_{j+1} Q^T
+  // runs on the matrix cores while the probabilities of tile j are formed;
+  // then O += V_j P_j runs while the row maxima of tile j + 1 are taken.
+  auto step = [&](int j, f32x16_t* cur, f32x16_t* nxt, auto parity) {
+    constexpr int PAR = decltype(parity)::value;  // j & 1
+    const bool more = j + 1 < ntiles;
+    if (more) issue_v(off_next, PAR ^ 1);
+    if (j + 2 < ntiles) {
+      off_next = page_off(j + 2);
+      issue_k(off_next, PAR);
+    }
+    if (wave_active) {
+      bf16x8_t pf[4];
+      // On the last tile this reads a stale slot; the result is not used, and
+      // keeping it unconditional lets the products overlap the exponentials.
+      qk(nxt, PAR ^ 1);
+      probs(cur, pf);
+      pv(pf, PAR);
+      rowsum(pf);
+      if (more) {
+        const int k1 = kb + (j + 1) * KV_TILE;
+        if (k1 + KV_TILE > wave_lim_min) mask(nxt, k1);
+        rebase(rowmax(nxt));
+      }
+    }
+    wait_memory_complete();
+    __syncthreads();
+    if (tail && j + 2 == ntiles) {  // V of the last tile has landed
+      zero_v_tail(PAR ^ 1, kb + (ntiles - 1) * KV_TILE);
+      __syncthreads();
+    }
+  };
+  for (int j = 0; j < ntiles; j += 2) {
+    step(j, sa, sb, std::integral_constant<int, 0>{});
+    if (j + 1 < ntiles) step(j + 1, sb, sa, std::integral_constant<int, 1>{});
   }
 
   l_run += shfl_xor(l_run, 32);
@@ -618,8 +702,8 @@ __device__ void decode_unit(const Args& a, const int32_t* it, char* wl) {
       *reinterpret_cast<u32x4_t*>(kl + R * 256 + ((x ^ ((R & 1) << 3)) << 4)) = k4[j];
       const int rg = q >> 2, si = q & 3;
       u32x4_t v = v4[j];
-      const int key0 = p * PAGE + 8 * (si & 1);
-      if (key0 + 8 > ke) v = mask_keys(v, key0, ke);
+      if (p * PAGE + PAGE > ke)
+        v = mask_elems(v, ke, [&](int e) { return p * PAGE + vt_pos(8 * (si & 1) + e); });
       *reinterpret_cast<u32x4_t*>(vl + rg * 64 + (((si + (rg >> 2)) & 3) << 4)) = v;
     }
     fetch(k4, v4, p + NSLOT);
@@ -674,8 +758,8 @@ __device__ void decode_unit(const Args& a, const int32_t* it, char* wl) {
       o0[h] *= alpha;
       o1[h] *= alpha;
       if (c == (h & 7)) {
-        pbuf[h * 16 + kg] = __builtin_bit_cast(uint16_t, (__bf16)p0);
-        pbuf[h * 16 + 8 + kg] = __builtin_bit_cast(uint16_t, (__bf16)p1);
+        pbuf[h * 16 + vt_pos(kg)] = __builtin_bit_cast(uint16_t, (__bf16)p0);
+        pbuf[h * 16 + vt_pos(8 + kg)] = __builtin_bit_cast(uint16_t, (__bf16)p1);
       }
       if constexpr (G >= 8) __builtin_amdgcn_sched_barrier(0);  // bound live ranges per head
     }

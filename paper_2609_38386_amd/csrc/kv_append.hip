@@ -5,11 +5,12 @@
 // One workgroup of 128 threads serves 16 consecutive packed tokens of one KV
 // head.  Keys keep their token-row layout: 16 threads copy one 256-byte row
 // with 16-byte loads and stores.  Values go into the transposed page
-// [dim][slot]: thread d gathers dimension d of the 16 tokens (256-byte
+// [dim][position], token slot t at position vt_pos(t) (slots 4-7 and 8-11
+// trade places): thread d gathers dimension d of the 16 tokens (256-byte
 // coalesced reads per token) and, when the 16 tokens fill one page in slot
 // order -- the common case inside a prefill chunk -- writes its whole 32-byte
 // row, so the workgroup stores the 4 KiB page contiguously.  Otherwise each
-// token's value lands with a 2-byte store at its slot.
+// token's value lands with a 2-byte store at its position.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -25,6 +26,9 @@ constexpr int D = DLFP_HEAD_DIM;
 constexpr int PAGE = DLFP_PAGE_SIZE;
 constexpr int TOK = 16;      // tokens per workgroup
 constexpr int THREADS = 128;
+
+// Position of token slot t in a value page row (bits 2 and 3 swap).
+__device__ __forceinline__ int vt_pos(int t) { return (t & 3) | ((t & 4) << 1) | ((t & 8) >> 1); }
 
 __global__ __launch_bounds__(THREADS) void kv_append_kernel(
     const uint16_t* __restrict__ k_new, const uint16_t* __restrict__ v_new,
@@ -60,9 +64,9 @@ __global__ __launch_bounds__(THREADS) void kv_append_kernel(
     const int64_t blk = s0 / PAGE;
     u32x4_t lo, hi;
 #pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      lo[w] = (uint32_t)vals[2 * w] | ((uint32_t)vals[2 * w + 1] << 16);
-      hi[w] = (uint32_t)vals[8 + 2 * w] | ((uint32_t)vals[8 + 2 * w + 1] << 16);
+    for (int w = 0; w < 4; ++w) {  // position p holds slot vt_pos(p)
+      lo[w] = (uint32_t)vals[vt_pos(2 * w)] | ((uint32_t)vals[vt_pos(2 * w + 1)] << 16);
+      hi[w] = (uint32_t)vals[vt_pos(8 + 2 * w)] | ((uint32_t)vals[vt_pos(8 + 2 * w + 1)] << 16);
     }
     u32x4_t* dst = reinterpret_cast<u32x4_t*>(v_cache + ((blk * hkv + h) * D + d) * PAGE);
     dst[0] = lo;
@@ -72,7 +76,7 @@ __global__ __launch_bounds__(THREADS) void kv_append_kernel(
       const int slot = slots[t0 + tt];
       if (slot < 0 || (int64_t)slot >= num_slots) continue;
       const int64_t blk = slot / PAGE, off = slot % PAGE;
-      v_cache[((blk * hkv + h) * D + d) * PAGE + off] = vals[tt];
+      v_cache[((blk * hkv + h) * D + d) * PAGE + vt_pos((int)off)] = vals[tt];
     }
   }
 }

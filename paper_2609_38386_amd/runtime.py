@@ -26,7 +26,8 @@ def device_to_bits(t: torch.Tensor) -> np.ndarray:
 
 
 class KVPool:
-    """Paged KV cache of one layer: K [nb][Hkv][16][128], V [nb][Hkv][128][16] (bf16)."""
+    """Paged KV cache of one layer: K [nb][Hkv][16][128], V [nb][Hkv][128][16] (bf16; the
+    value page is transposed with slots 4-7 and 8-11 trading places)."""
 
     def __init__(self, num_blocks: int, num_kv_heads: int, device, fill_bits: Optional[int] = None):
         shape_k = (num_blocks, num_kv_heads, _d.PAGE_SIZE, _d.HEAD_DIM)

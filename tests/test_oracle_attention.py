@@ -63,7 +63,7 @@ def _scatter(logical_k, logical_v, block_row, pool_blocks):
     for j in range(n):
         b = block_row[j // 16]
         kc[b, :, j % 16, :] = logical_k[j]
-        vc[b, :, :, j % 16] = logical_v[j]
+        vc[b, :, :, paging.value_position(j % 16)] = logical_v[j]
     return kc, vc
 
 
@@ -76,7 +76,7 @@ def test_gather_hand_example():
         for h in range(hkv):
             for t in range(16):
                 kc[b, h, t, :] = 1000 * b + 100 * h + t
-                vc[b, h, :, t] = 1000 * b + 100 * h + t + 50
+                vc[b, h, :, paging.value_position(t)] = 1000 * b + 100 * h + t + 50
     k, v = paging.gather_sequence(kc, vc, np.array([3, 1]), 20)
     # token 0 -> block 3 slot 0; token 15 -> block 3 slot 15; token 17 -> block 1 slot 1
     assert k[0, 0, 0] == 3000 and k[15, 1, 2] == 3115 and k[17, 0, 1] == 1001
