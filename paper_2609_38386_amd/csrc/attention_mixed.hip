@@ -510,6 +510,21 @@ __device__ void prefill_unit(const Args& a, const int32_t* it, char* smem, int* 
       probs(cur, pf);
       pv(pf, PAR);
       rowsum(pf);
+      // Issue order: QK(j+1) products interleaved with the exponentials, then
+      // PV(j) products interleaved with the row sums.
+      __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
       if (more) {
         const int k1 = kb + (j + 1) * KV_TILE;
         if (k1 + KV_TILE > wave_lim_min) mask(nxt, k1);
