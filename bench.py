@@ -30,6 +30,7 @@ import time
 
 import numpy as np
 
+ROOT = os.path.dirname(os.path.abspath(__file__))
 HBM_PEAK_GBS = 8000.0
 MFMA_BF16_PEAK_TFLOPS = 2500.0
 METRIC = "mixed-iteration latency vs prefill chunk; decode HBM GB/s %peak; prefill MFMA %"
@@ -206,6 +207,31 @@ class Sweep:
         return sorted({0, iters // 2, iters - 1})
 
 
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "attention_mixed_qwen3-0.6b_sweep_hbm_traffic.md")
+KERNEL_SOURCES = ("paper_2609_38386_amd/csrc/attention_mixed.hip", "include/dlfp.h",
+                  "paper_2609_38386_amd/csrc/dlfp_internal.h")
+
+
+def profiled_traffic():
+    """HBM bytes per attention launch of the sweep from the committed FETCH_SIZE /
+    WRITE_SIZE summary (calibrated against a device copy), or None when the kernel
+    sources have changed since the counters were taken."""
+    import hashlib
+    try:
+        text = open(TRAFFIC_PROFILE).read()
+        h = hashlib.sha256()
+        for f in KERNEL_SOURCES:
+            with open(os.path.join(ROOT, f), "rb") as fh:
+                h.update(fh.read())
+    except OSError:
+        return None
+    fields = dict(line.split(": ", 1) for line in text.splitlines()
+                  if line.startswith(("traffic_bytes_per_launch: ", "source_sha256: ")))
+    if fields.get("source_sha256", "").strip() != h.hexdigest():
+        return None
+    return int(fields["traffic_bytes_per_launch"])
+
+
 def run_headline(args, dev, log_fn):
     import torch
     from paper_2609_38386_amd import dlfp as D
@@ -263,9 +289,10 @@ def run_headline(args, dev, log_fn):
             "controller_cap_last": s["caps"][-1],
         }
     avg_launch_s = attn_ms * 1e-3 / n_launch
+    traffic = profiled_traffic()
     ach = (bytes_all / n_launch) / avg_launch_s / 1e9
     roofline = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None,
+                "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": traffic,
                 "kernel": "attention_mixed_kernel<2>",
                 "avg_launch_us": round(avg_launch_s * 1e6, 2),
                 "algorithmic_bytes_per_launch": int(bytes_all / n_launch),
