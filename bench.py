@@ -130,7 +130,9 @@ class Sweep:
             self.inputs[p] = (q, k, v)
         max_tok = max(cfg.chunks) + self.n
         self.out = torch.empty((max_tok, self.hq, 128), dtype=torch.bfloat16, device=dev)
-        self.stage = rt.StagedBatch(self.dims, self.n + 1, max_tok, 65536, dev)
+        # two staging slots: the next iteration's metadata is built while one runs
+        self.stages = [rt.StagedBatch(self.dims, self.n + 1, max_tok, 65536, dev) for _ in range(2)]
+        self.stage = self.stages[0]
         self.ws = rt.Workspace(dev, 64 << 20)
         self.timer = D.Timer()
         self.ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
@@ -146,9 +148,11 @@ class Sweep:
         self.pool_ptrs = [(ctypes.c_void_p(pl.k.data_ptr()), ctypes.c_void_p(pl.v.data_ptr()))
                           for pl in self.pools]
 
-    def iteration(self, p, c, ctrl=None, decoders=True, prefill=True, record=True):
-        """Run one mixed iteration; returns (device ms, [attention ms per layer], q_len, kv_len)."""
-        torch, D = self.torch, self.D
+    def prepare(self, p, c, decoders=True, prefill=True, slot=0):
+        """Host side of one mixed iteration: its metadata, built into staging slot
+        `slot` and copied to the device on the stream (ordered after whatever was
+        enqueued before, so it can be built while the previous iteration runs)."""
+        torch = self.torch
         q_len, kv_len, rows = [], [], []
         if prefill:
             q_len.append(p)
@@ -162,12 +166,21 @@ class Sweep:
         kv_len = np.asarray(kv_len, dtype=np.int32)
         bt = self.bt if (prefill and decoders) else np.ascontiguousarray(self.bt[rows])
         d_bt = self.d_bt if (prefill and decoders) else torch.from_numpy(bt).to(self.dev)
-        st = self.stage.build(q_len, kv_len, bt, self.num_blocks)
+        st = self.stages[slot].build(q_len, kv_len, bt, self.num_blocks)
         T = st.num_tokens
         qa, ka, va = self.inputs[p]
         base = c * (p + self.n)
         lo = base if prefill else base + p
-        q, k, v = qa[lo:lo + T], ka[lo:lo + T], va[lo:lo + T]
+        return {"q_len": q_len, "kv_len": kv_len, "bt": bt, "d_bt": d_bt, "st": st, "T": T,
+                "qkv": (qa[lo:lo + T], ka[lo:lo + T], va[lo:lo + T]),
+                "guarded": bool(prefill and decoders), "decoders": decoders}
+
+    def launch(self, pr, record=True):
+        """Enqueue the layers of a prepared iteration between the completion timer's
+        events; with `record`, HIP events also bracket every attention launch."""
+        D = self.D
+        st, T, bt, d_bt = pr["st"], pr["T"], pr["bt"], pr["d_bt"]
+        q, k, v = pr["qkv"]
         meta = st.meta
         ws = self.ws.ensure(meta.workspace_bytes)
         ct, vp = self.ct, self.ct.c_void_p
@@ -194,11 +207,22 @@ class Sweep:
             if record:
                 self.ev[layer][1].record(self.stream)
         self.timer.stop(self.stream)
-        ms = self.timer.elapsed_ms()          # completion: waits for the iteration to finish
-        attn = [a.elapsed_time(b) for a, b in self.ev] if record else []
+        pr["record"] = record
+
+    def finish(self, pr, ctrl=None):
+        """Wait for the iteration (completion timing), step the controller from the
+        measured latency; returns (device ms, [attention ms per layer], q_len, kv_len)."""
+        ms = self.timer.elapsed_ms()
+        attn = [a.elapsed_time(b) for a, b in self.ev] if pr["record"] else []
         if ctrl is not None:
-            D.dlfp_controller_step(ctrl, self.n if decoders else 0, bool(prefill and decoders), ms)
-        return ms, attn, q_len, kv_len
+            self.D.dlfp_controller_step(ctrl, self.n if pr["decoders"] else 0, pr["guarded"], ms)
+        return ms, attn, pr["q_len"], pr["kv_len"]
+
+    def iteration(self, p, c, ctrl=None, decoders=True, prefill=True, record=True):
+        """Prepare, launch and finish one mixed iteration."""
+        pr = self.prepare(p, c, decoders, prefill)
+        self.launch(pr, record)
+        return self.finish(pr, ctrl)
 
     def chunks(self, p, policy):
         iters = self.cfg.prompt_len // p
@@ -232,6 +256,13 @@ def profiled_traffic():
     return int(fields["traffic_bytes_per_launch"])
 
 
+def recorded(cfg, p, c):
+    """Iterations of the timed sweep whose attention launches are bracketed by HIP
+    events: every fourth chunk iteration of each chunk size (chunks 3, 7, 11, ...),
+    a quarter of the sweep in its own mix of chunk sizes."""
+    return c % 4 == 3
+
+
 def run_headline(args, dev, log_fn):
     import torch
     from paper_2609_38386_amd import dlfp as D
@@ -245,20 +276,33 @@ def run_headline(args, dev, log_fn):
     target = 1.2 * float(np.median(dec_ms))
     ctrl = D.dlfp_controller_init(target, 2048, 32, 4096, 128)
 
+    iters = [(p, c) for p in cfg.chunks for c in sw.chunks(p, "all")]
+
     def step(stats):
-        for p in cfg.chunks:
-            for c in sw.chunks(p, "all"):
-                ms, attn, ql, kl = sw.iteration(p, c, ctrl=ctrl)
-                if stats is not None:
-                    s = stats.setdefault(p, {"iter_ms": [], "attn_ms": 0.0, "bytes": 0, "flops": 0,
-                                             "tokens": 0, "caps": []})
-                    s["iter_ms"].append(ms)
-                    s["attn_ms"] += sum(attn)
-                    db, pb, df, pf = attn_work(sw.hq, sw.hkv, ql, kl)
-                    s["bytes"] += (db + pb) * cfg.layers
-                    s["flops"] += (df + pf) * cfg.layers
-                    s["tokens"] += int(ql.sum())
-                    s["caps"].append(ctrl.cap)
+        # The next iteration's metadata is built while the current one runs; the
+        # controller is stepped from each iteration's completion time.  HIP events
+        # bracket the attention launches of the sampled iterations only (each event
+        # pair adds a dispatch gap of several microseconds to a layer).
+        pr = sw.prepare(*iters[0], slot=0)
+        for i, (p, c) in enumerate(iters):
+            rec = recorded(cfg, p, c)
+            sw.launch(pr, record=rec)
+            nxt = sw.prepare(*iters[i + 1], slot=(i + 1) & 1) if i + 1 < len(iters) else None
+            ms, attn, ql, kl = sw.finish(pr, ctrl)
+            pr = nxt
+            if stats is None:
+                continue
+            s = stats.setdefault(p, {"iter_ms": [], "attn_ms": 0.0, "bytes": 0, "flops": 0,
+                                     "tokens": 0, "caps": [], "recorded": 0})
+            s["iter_ms"].append(ms)
+            s["tokens"] += int(ql.sum())
+            s["caps"].append(ctrl.cap)
+            if rec:
+                s["recorded"] += 1
+                s["attn_ms"] += sum(attn)
+                db, pb, df, pf = attn_work(sw.hq, sw.hkv, ql, kl)
+                s["bytes"] += (db + pb) * cfg.layers
+                s["flops"] += (df + pf) * cfg.layers
 
     for _ in range(args.warmup):
         step(None)
@@ -271,13 +315,13 @@ def run_headline(args, dev, log_fn):
     wall = time.perf_counter() - t_start
     tokens = sum(s["tokens"] for s in stats.values())
     attn_ms = sum(s["attn_ms"] for s in stats.values())
-    n_launch = sum(len(s["iter_ms"]) for s in stats.values()) * cfg.layers
+    n_launch = sum(s["recorded"] for s in stats.values()) * cfg.layers
     bytes_all = sum(s["bytes"] for s in stats.values())
     flops_all = sum(s["flops"] for s in stats.values())
     latency = {}
     for p, s in stats.items():
         it = np.asarray(s["iter_ms"])
-        per_launch_ms = s["attn_ms"] / (len(it) * cfg.layers)
+        per_launch_ms = s["attn_ms"] / (s["recorded"] * cfg.layers)
         latency[str(p)] = {
             "iter_ms_mean": round(float(it.mean()), 4), "iter_ms_p50": round(float(np.median(it)), 4),
             "iter_ms_p90": round(float(np.percentile(it, 90)), 4),
@@ -286,6 +330,7 @@ def run_headline(args, dev, log_fn):
             "attn_TFLOPs": round(s["flops"] / (s["attn_ms"] * 1e-3) / 1e12, 1),
             "ttft_proxy_ms": round(float(it.sum()) / args.steps, 3),
             "iterations": len(it) // args.steps,
+            "iterations_with_launch_events": s["recorded"] // args.steps,
             "controller_cap_last": s["caps"][-1],
         }
     avg_launch_s = attn_ms * 1e-3 / n_launch

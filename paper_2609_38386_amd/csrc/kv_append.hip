@@ -39,27 +39,42 @@ __global__ __launch_bounds__(THREADS) void kv_append_kernel(
   const int tid = threadIdx.x;
   const int nt = min(TOK, num_tokens - t0);
 
-  // Keys: 16 tokens x 16 chunks of 16 bytes.
-  for (int i = tid; i < nt * 16; i += THREADS) {
-    const int tt = i >> 4, c = i & 15;
-    const int slot = slots[t0 + tt];
-    if (slot < 0 || (int64_t)slot >= num_slots) continue;
-    const int64_t blk = slot / PAGE, off = slot % PAGE;
-    const u32x4_t v = *reinterpret_cast<const u32x4_t*>(
-        k_new + ((int64_t)(t0 + tt) * hkv + h) * D + c * 8);
-    *reinterpret_cast<u32x4_t*>(k_cache + ((blk * hkv + h) * PAGE + off) * D + c * 8) = v;
+  // Every load is issued before any store (one memory round trip): the
+  // workgroup's slots, two 16-byte key chunks per thread (tokens tid / 16 and
+  // tid / 16 + 8, chunk tid % 16) and the 16 values of dimension d = tid.
+  int sl[TOK];
+#pragma unroll
+  for (int tt = 0; tt < TOK; ++tt) sl[tt] = tt < nt ? slots[t0 + tt] : -1;
+  const int c = tid & 15;
+  u32x4_t kv[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int tt = (tid >> 4) + 8 * j;
+    kv[j] = tt < nt ? *reinterpret_cast<const u32x4_t*>(k_new + ((int64_t)(t0 + tt) * hkv + h) * D + c * 8)
+                    : u32x4_t{0u, 0u, 0u, 0u};
   }
-
-  // Values: thread d owns dimension d.
   const int d = tid;
   uint16_t vals[TOK];
 #pragma unroll
   for (int tt = 0; tt < TOK; ++tt)
     vals[tt] = tt < nt ? v_new[((int64_t)(t0 + tt) * hkv + h) * D + d] : 0;
-  const int s0 = slots[t0];
+
+  // Keys: token rows, 16-byte chunks.
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int tt = (tid >> 4) + 8 * j;
+    const int slot = sl[tt];
+    if (tt < nt && slot >= 0 && (int64_t)slot < num_slots) {
+      const int64_t blk = slot / PAGE, off = slot % PAGE;
+      *reinterpret_cast<u32x4_t*>(k_cache + ((blk * hkv + h) * PAGE + off) * D + c * 8) = kv[j];
+    }
+  }
+
+  // Values: thread d owns dimension d.
+  const int s0 = sl[0];
   bool full = nt == TOK && s0 >= 0 && (int64_t)s0 + TOK <= num_slots && (s0 % PAGE) == 0;
 #pragma unroll
-  for (int tt = 1; tt < TOK; ++tt) full = full && (tt >= nt || slots[t0 + tt] == s0 + tt);
+  for (int tt = 1; tt < TOK; ++tt) full = full && sl[tt] == s0 + tt;
   if (full) {
     const int64_t blk = s0 / PAGE;
     u32x4_t lo, hi;
@@ -72,11 +87,13 @@ __global__ __launch_bounds__(THREADS) void kv_append_kernel(
     dst[0] = lo;
     dst[1] = hi;
   } else {
-    for (int tt = 0; tt < nt; ++tt) {
-      const int slot = slots[t0 + tt];
-      if (slot < 0 || (int64_t)slot >= num_slots) continue;
-      const int64_t blk = slot / PAGE, off = slot % PAGE;
-      v_cache[((blk * hkv + h) * D + d) * PAGE + vt_pos((int)off)] = vals[tt];
+#pragma unroll
+    for (int tt = 0; tt < TOK; ++tt) {
+      const int slot = sl[tt];
+      if (tt < nt && slot >= 0 && (int64_t)slot < num_slots) {
+        const int64_t blk = slot / PAGE, off = slot % PAGE;
+        v_cache[((blk * hkv + h) * D + d) * PAGE + vt_pos((int)off)] = vals[tt];
+      }
     }
   }
 }
