@@ -141,7 +141,7 @@ enum {
   DLFP_W_SPLIT = 7,    /* index of this split within the group */
   DLFP_W_NSPLITS = 8,  /* splits in the group */
   DLFP_W_WSOFF = 9,    /* float offset of this unit's partial result in the workspace; a
-                          slot holds O[rows][128], m[rows], l[rows] (rows = tokens x g),
+                          slot holds O (rows x 128 floats), m[rows], l[rows] (rows = tokens x g),
                           padded to a multiple of 64 floats */
   DLFP_W_WSGROUP = 10, /* float offset of the group's split 0 partial */
   DLFP_W_KIND = 11     /* DLFP_KIND_PREFILL or DLFP_KIND_DECODE */

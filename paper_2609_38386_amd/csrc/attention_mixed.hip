@@ -180,7 +180,7 @@ __device__ __forceinline__ float pload1(Slots s, int float_off) {
   return __builtin_bit_cast(float,
                             __builtin_amdgcn_raw_buffer_load_b32(s.r, float_off * 4, 0, CPOL_SC1));
 }
-// Floats per partial slot: O[rows][128], m[rows], l[rows], padded to 256 bytes.
+// Floats per partial slot: O (rows x 128), m[rows], l[rows], padded to 256 bytes.
 __device__ __forceinline__ int slot_floats_for(int rows) {
   return (rows * (D + 2) + 63) / 64 * 64;
 }
@@ -560,7 +560,10 @@ __device__ void prefill_unit(const Args& a, const int32_t* it, char* smem, int* 
     return;
   }
 
-  // Partial result: O[rows][128], then m[rows], then l[rows].
+  // Partial result: O as 16 chunks c = 4 mb + g4 of [rows][2][4] floats (chunk
+  // c, row r, half h holds dims 32 mb + 8 g4 + 4 h .. + 3), so that a wave's
+  // store and the merge's loads each cover a contiguous kilobyte; then
+  // m[rows] and l[rows].
   const int slot_floats = slot_floats_for(rows);
   const Slots sl = group_slots(a.ws, it[DLFP_W_WSGROUP], nsplits, slot_floats);
   const int my = it[DLFP_W_SPLIT] * slot_floats;
@@ -571,7 +574,7 @@ __device__ void prefill_unit(const Args& a, const int32_t* it, char* smem, int* 
       for (int g4 = 0; g4 < 4; ++g4) {
         const f32x4_t v = {o[mb][4 * g4], o[mb][4 * g4 + 1], o[mb][4 * g4 + 2],
                            o[mb][4 * g4 + 3]};
-        pstore4(sl, my + r * D + mb * 32 + 8 * g4 + 4 * hi, v);
+        pstore4(sl, my + ((4 * mb + g4) * rows + r) * 8 + 4 * hi, v);
       }
     if (hi == 0) {
       pstore1(sl, my + rows * D + r, m_run);
@@ -586,49 +589,55 @@ __device__ void prefill_unit(const Args& a, const int32_t* it, char* smem, int* 
   if (!*flag) return;
 
   // Last arriver: merge every split of the group in split order with an
-  // online rescale.  Four threads per row, 32 dims each, two passes over the
-  // rows; the loads of four splits are issued before any is consumed, so a
-  // pass costs about one memory round trip per four splits.
-  for (int row = tid >> 2; row < rows; row += THREADS / 4) {
-    const int quarter = tid & 3;
-    float M = NEG_BIG, lsum = 0.f;
-    f32x4_t acc[8];
+  // online rescale.  Two threads per row (thread t: row t / 2, half t % 2) and
+  // two passes over the 16 chunks of O; the loads of four splits are issued
+  // before any is consumed, so a pass costs about one memory round trip per
+  // four splits, and every load instruction reads a contiguous kilobyte.
+  if (tid < 2 * rows) {
+    const int row = tid >> 1, h = tid & 1;
+    const int trow = row / G, hrow = row % G;
+    const int64_t orow = ((int64_t)(q0 + t0 + trow) * a.hq + kh * G + hrow) * D;
+    for (int pass = 0; pass < 2; ++pass) {
+      float M = NEG_BIG, lsum = 0.f;
+      f32x4_t acc[8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) acc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    for (int j = 0; j < nsplits; j += 4) {
-      float mj[4], lj[4];
-      f32x4_t x[4][8];
+      for (int i = 0; i < 8; ++i) acc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      for (int j = 0; j < nsplits; j += 4) {
+        float mj[4], lj[4];
+        f32x4_t x[4][8];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int b = min(j + u, nsplits - 1) * slot_floats;
-        mj[u] = pload1(sl, b + rows * D + row);
-        lj[u] = pload1(sl, b + rows * D + rows + row);
+        for (int u = 0; u < 4; ++u) {
+          const int b = min(j + u, nsplits - 1) * slot_floats;
+          mj[u] = pload1(sl, b + rows * D + row);
+          lj[u] = pload1(sl, b + rows * D + rows + row);
 #pragma unroll
-        for (int i = 0; i < 8; ++i) x[u][i] = pload4(sl, b + row * D + quarter * 32 + 4 * i);
+          for (int i = 0; i < 8; ++i) x[u][i] = pload4(sl, b + ((8 * pass + i) * rows + row) * 8 + 4 * h);
+        }
+        float mn = M;
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          if (j + u < nsplits) mn = fmaxf(mn, mj[u]);
+        const float rs = fexp2(M - mn);
+        M = mn;
+        lsum *= rs;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[i] *= rs;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const float w = j + u < nsplits ? fexp2(mj[u] - mn) : 0.f;
+          lsum += w * lj[u];
+#pragma unroll
+          for (int i = 0; i < 8; ++i) acc[i] += w * x[u][i];
+        }
       }
-      float mn = M;
+      const float inv = 1.f / lsum;
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
-        if (j + u < nsplits) mn = fmaxf(mn, mj[u]);
-      const float r = fexp2(M - mn);
-      M = mn;
-      lsum *= r;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) acc[i] *= r;
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const float w = j + u < nsplits ? fexp2(mj[u] - mn) : 0.f;
-        lsum += w * lj[u];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) acc[i] += w * x[u][i];
+      for (int i = 0; i < 8; ++i) {  // chunk 8 pass + i: mb = 2 pass + i / 4, g4 = i % 4
+        const int dim = 32 * (2 * pass + (i >> 2)) + 8 * (i & 3) + 4 * h;
+        store4(a, orow + dim, acc[i][0] * inv, acc[i][1] * inv, acc[i][2] * inv,
+               acc[i][3] * inv);
       }
     }
-    const float inv = 1.f / lsum;
-    const int trow = row / G, hrow = row % G;
-    const int64_t orow = ((int64_t)(q0 + t0 + trow) * a.hq + kh * G + hrow) * D + quarter * 32;
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-      store4(a, orow + 4 * i, acc[i][0] * inv, acc[i][1] * inv, acc[i][2] * inv, acc[i][3] * inv);
   }
   if (tid == 0)
     __hip_atomic_store(group_counter(a.ws, grp), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

@@ -20,7 +20,7 @@ int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
 // Prefill key ranges start on a 64-key tile.
 constexpr int64_t KV_GRANULE_PREFILL = 64;
 
-// Floats of one partial result: O[rows][128], m[rows], l[rows], padded to 256 bytes.
+// Floats of one partial result: O (rows x 128), m[rows], l[rows], padded to 256 bytes.
 int64_t slot_floats(int64_t rows) { return round_up(rows * (DLFP_HEAD_DIM + 2), 64); }
 
 struct Unit {
