@@ -94,7 +94,7 @@ typedef struct {
 
 /* How the attention launch splits key ranges (split-K).  Zero fields pick
  * the built-in policy: prefill key ranges are cut so the prefill share offers
- * about one unit per resident workgroup (never below 1024 keys), decode
+ * about one unit per compute unit (never below 1024 keys), decode
  * ranges into sqrt(256 W / F) keys for W decode keys over the F resident
  * wavefronts the prefill units leave free, and a range longer than its split
  * is cut into equal parts. */

@@ -117,12 +117,13 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
   if (tokens > std::numeric_limits<int32_t>::max()) return DLFP_ERANGE;
 
   // Prefill split: long key ranges are cut so that the prefill share offers
-  // about one unit per resident workgroup (four wavefronts), never below 1024
-  // keys.
+  // about one unit per compute unit (eight resident wavefronts; two prefill
+  // workgroups sharing a CU each run at little more than half speed), never
+  // below 1024 keys.
   int64_t split_p = tn.prefill_split_tokens;
   if (!split_p)
     split_p = std::clamp<int64_t>(
-        round_up(std::max<int64_t>(1, ceil_div(pre_keys, std::max<int64_t>(1, resident / 4))), 64),
+        round_up(std::max<int64_t>(1, ceil_div(pre_keys, std::max<int64_t>(1, resident / 8))), 64),
         1024, DLFP_MAX_PREFILL_UNIT_KEYS);
   // Decode split.  The launch time is roughly the share of work per resident
   // wavefront plus the longest unit, and every unit adds a fixed cost (query
