@@ -67,11 +67,17 @@ extern "C" {
 #define DLFP_MAX_PREFILL_UNIT_KEYS 32768
 /* int32 fields per work unit (see dlfp_build_varlen_meta). */
 #define DLFP_WORK_INTS 16
-/* Workspace layout: a 256-byte header (word 0 = error flag), then a fixed
- * region of DLFP_MAX_GROUPS int32 split counters, then partial results from
- * byte DLFP_WORKSPACE_PARTIALS on.  The counter region has the same size for
- * every launch, so one workspace can serve iterations of any shape. */
+/* Workspace layout: a 256-byte header (int32 word 0 = error flag, word
+ * DLFP_WORKSPACE_TICKET_WORD = the decode queue's next ticket, word
+ * DLFP_WORKSPACE_DONE_WORD = decode workgroups finished; both are zero
+ * between launches), then a fixed region of DLFP_MAX_GROUPS int32 split
+ * counters, then partial results from byte DLFP_WORKSPACE_PARTIALS on.  The
+ * counter region has the same size for every launch, so one workspace can
+ * serve iterations of any shape.  A launch that did not complete (a device
+ * fault) leaves the header undefined: initialise the workspace again. */
 #define DLFP_WORKSPACE_HEADER 256
+#define DLFP_WORKSPACE_TICKET_WORD 16
+#define DLFP_WORKSPACE_DONE_WORD 32
 #define DLFP_MAX_GROUPS 65536
 #define DLFP_WORKSPACE_PARTIALS (DLFP_WORKSPACE_HEADER + 4 * DLFP_MAX_GROUPS)
 

@@ -36,6 +36,7 @@
 // the counter to zero for the next launch.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdint>
 #include <type_traits>
 
@@ -87,7 +88,8 @@ struct Args {
   int32_t num_units;
   int32_t num_prefill;
   int32_t out_f32;
-  float scale_log2;  // softmax scale * log2(e)
+  int32_t decode_waves;  // wavefronts of the decode workgroups of this launch
+  float scale_log2;      // softmax scale * log2(e)
 };
 
 __device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
@@ -131,6 +133,12 @@ __device__ __forceinline__ void wave_sync() {
 __device__ __forceinline__ int* group_counter_ptr(float* ws, int grp) {
   return reinterpret_cast<int*>(reinterpret_cast<char*>(ws) + DLFP_WORKSPACE_HEADER) + grp;
 }
+
+// Header words of the workspace: the decode queue's next ticket and the
+// count of decode wavefronts that found it empty.
+__device__ __forceinline__ int* header_word(float* ws, int i) { return reinterpret_cast<int*>(ws) + i; }
+constexpr int HDR_TICKET = DLFP_WORKSPACE_TICKET_WORD;
+constexpr int HDR_DONE = DLFP_WORKSPACE_DONE_WORD;
 
 __device__ __forceinline__ void raise_error(float* ws) {
   __hip_atomic_store(reinterpret_cast<int*>(ws), 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -928,16 +936,60 @@ __global__ __launch_bounds__(THREADS, 2) void attention_mixed_kernel(Args a) {
     const int u = xcd_remap(b, a.num_prefill);
     prefill_unit<G>(a, a.work + (int64_t)u * DLFP_WORK_INTS, smem, &flag);
   } else {
-    const int wave = threadIdx.x >> 6;
-    const int u = a.num_prefill + (b - a.num_prefill) * 4 + wave;
-    if (u >= a.num_units) return;
-    decode_unit<G>(a, a.work + (int64_t)u * DLFP_WORK_INTS, smem + wave * DEC_WAVE_LDS);
+    // Decode wavefront w of decode workgroup d starts with unit 4 d + w; when
+    // there are more units than wavefronts, the rest form a queue that
+    // wavefronts drain one ticket at a time as they finish, so none idles while
+    // units remain (a workgroup's slot frees only when all four of its
+    // wavefronts are done).  The last workgroup to finish resets the header
+    // words for the next launch.
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    char* wl = smem + wave * DEC_WAVE_LDS;
+    const int ndec = a.num_units - a.num_prefill;
+    const bool queue = ndec > a.decode_waves;
+    int t = (b - a.num_prefill) * 4 + wave;
+    while (t < ndec) {
+      decode_unit<G>(a, a.work + (int64_t)(a.num_prefill + t) * DLFP_WORK_INTS, wl);
+      wave_sync();
+      if (!queue) break;
+      int nt = 0;
+      if (lane == 0)
+        nt = a.decode_waves + __hip_atomic_fetch_add(header_word(a.ws, HDR_TICKET), 1,
+                                                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      t = uniform(__shfl(nt, 0));
+    }
+    if (queue) {
+      __syncthreads();
+      if (threadIdx.x == 0) {
+        const int d = __hip_atomic_fetch_add(header_word(a.ws, HDR_DONE), 1, __ATOMIC_RELAXED,
+                                             __HIP_MEMORY_SCOPE_AGENT);
+        if (d == a.decode_waves / 4 - 1) {
+          __hip_atomic_store(header_word(a.ws, HDR_TICKET), 0, __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
+          __hip_atomic_store(header_word(a.ws, HDR_DONE), 0, __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
+        }
+      }
+    }
   }
 }
 
 __global__ void fill_zero_kernel(int* p, int64_t n) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) p[i] = 0;
+}
+
+// Compute units of the current device (queried once per device).
+int compute_units() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (!cached[dev]) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+      n = 256;
+    cached[dev] = n;
+  }
+  return cached[dev];
 }
 
 template <int G>
@@ -993,8 +1045,12 @@ extern "C" int dlfp_attention_mixed(const dlfp_dims* dims, const dlfp_meta* meta
   a.num_prefill = meta->num_prefill_units;
   a.out_f32 = out_dtype;
   a.scale_log2 = scale * LOG2E;
+  // Decode workgroups: enough to fill the resident slots of the device (two
+  // per CU), fewer when there are fewer units; they drain the decode queue.
   const int decode_units = meta->num_units - meta->num_prefill_units;
-  const int grid = meta->num_prefill_units + (decode_units + 3) / 4;
+  const int decode_wgs = std::min((decode_units + 3) / 4, 2 * compute_units());
+  a.decode_waves = 4 * decode_wgs;
+  const int grid = meta->num_prefill_units + decode_wgs;
   (void)hipGetLastError();
   hipError_t e;
   switch (g) {

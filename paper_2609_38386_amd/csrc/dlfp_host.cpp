@@ -209,6 +209,10 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
     for (int kh = 0; kh < hkv; ++kh)
       emit(s, kh, 0, 1, kv_len[s], split_d, DLFP_PAGE_SIZE, DLFP_KIND_DECODE);
   }
+  // Decode wavefronts take units in list order from a queue: longest first.
+  std::stable_sort(units.begin() + num_prefill, units.end(), [](const Unit& x, const Unit& y) {
+    return x.f[DLFP_W_KVEND] - x.f[DLFP_W_KVBEGIN] > y.f[DLFP_W_KVEND] - y.f[DLFP_W_KVBEGIN];
+  });
   if ((int64_t)units.size() > std::numeric_limits<int32_t>::max() / DLFP_WORK_INTS)
     return DLFP_ERANGE;
   if (groups > DLFP_MAX_GROUPS) return DLFP_ERANGE;
@@ -218,7 +222,7 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
   std::vector<int64_t> group_off(groups, 0);
   int64_t off = partial_base_bytes / 4;
   {
-    // assign in order of first appearance (units are grouped contiguously)
+    // assign in order of first appearance
     std::vector<int64_t> seen(groups, -1);
     for (const Unit& u : units) {
       const int32_t grp = u.f[DLFP_W_GROUP];
