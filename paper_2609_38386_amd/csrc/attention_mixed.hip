@@ -118,6 +118,38 @@ constexpr int DPP_ROR8 = 0x128;        // rotate a 16-lane row by 8
 
 __device__ __forceinline__ float shfl_xor(float x, int m) { return __shfl_xor(x, m); }
 
+// Combine a value with the one of lane ^ 16 (or lane ^ 32) by the gfx950
+// permlane swaps (VALU, no LDS round trip): swapping two copies of a value
+// leaves the lane's own value in one register and its partner's in the
+// other.  Written as assembly because the compiler reads both results of
+// the swap builtin from one register, losing the partner's value.
+__device__ __forceinline__ void swap16(float& a, float& b) {
+  asm volatile("s_nop 1\n\tv_permlane16_swap_b32 %0, %1" : "+v"(a), "+v"(b));
+}
+__device__ __forceinline__ void swap32(float& a, float& b) {
+  asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1" : "+v"(a), "+v"(b));
+}
+__device__ __forceinline__ float max_xor16(float x) {
+  float a = x, b = x;
+  swap16(a, b);
+  return fmaxf(a, b);
+}
+__device__ __forceinline__ float max_xor32(float x) {
+  float a = x, b = x;
+  swap32(a, b);
+  return fmaxf(a, b);
+}
+__device__ __forceinline__ float sum_xor16(float x) {
+  float a = x, b = x;
+  swap16(a, b);
+  return a + b;
+}
+__device__ __forceinline__ float sum_xor32(float x) {
+  float a = x, b = x;
+  swap32(a, b);
+  return a + b;
+}
+
 __device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
 // Lanes of one wavefront hand data to each other through LDS.  The hardware
@@ -420,9 +452,7 @@ __device__ void prefill_unit(const Args& a, const int32_t* it, char* smem, int* 
     for (int kb2 = 0; kb2 < 2; ++kb2)
 #pragma unroll
       for (int rr = 0; rr < 16; ++rr) mx = fmaxf(mx, sacc[kb2][rr]);
-    const auto sw = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(int, mx),
-                                                     __builtin_bit_cast(int, mx), false, false);
-    return fmaxf(__builtin_bit_cast(float, sw[0]), __builtin_bit_cast(float, sw[1]));
+    return max_xor32(mx);
   };
   // Raise the reference maximum where a tile exceeds it by more than
   // RESCALE_LOG2 (scaled units); the accumulators follow.
@@ -551,7 +581,7 @@ __device__ void prefill_unit(const Args& a, const int32_t* it, char* smem, int* 
     if (j + 1 < ntiles) step(j + 1, sb, sa, std::integral_constant<int, 1>{});
   }
 
-  l_run += shfl_xor(l_run, 32);
+  l_run = sum_xor32(l_run);
   const int rows = nt * G;
   // o[mb][rr] = O[row][32 mb + 8 (rr / 4) + 4 hi + rr % 4]
   if (nsplits == 1) {
@@ -780,8 +810,8 @@ __device__ void decode_unit(const Args& a, const int32_t* it, char* wl) {
       sc[1] = valid1 ? sc[1] : -__builtin_inff();
       float mx = fmaxf(sc[0], sc[1]);
       mx = fmaxf(mx, dpp<DPP_ROR8>(mx));
-      mx = fmaxf(mx, shfl_xor(mx, 16));
-      mx = fmaxf(mx, shfl_xor(mx, 32));
+      mx = max_xor16(mx);
+      mx = max_xor32(mx);
       const float m_new = fmaxf(m[h], mx);
       const float alpha = fexp2(m[h] - m_new);
       m[h] = m_new;
@@ -835,8 +865,8 @@ __device__ void decode_unit(const Args& a, const int32_t* it, char* wl) {
   for (int h = 0; h < G; ++h) {
     float x = l[h];
     x += dpp<DPP_ROR8>(x);
-    x += shfl_xor(x, 16);
-    x += shfl_xor(x, 32);
+    x = sum_xor16(x);
+    x = sum_xor32(x);
     l[h] = __builtin_bit_cast(float, uniform(__builtin_bit_cast(int, x)));
   }
 

@@ -256,3 +256,28 @@ def test_workspace_reuse_across_iteration_shapes(dev):
         _compare(_to64(b.run(w, SCALE, torch.float32)), big, "reuse big")
     torch.cuda.synchronize()
     assert not w.buf[:D.WORKSPACE_PARTIALS].view(torch.int32).cpu().numpy().any()
+
+
+@pytest.mark.parametrize("g", [2, 8])
+def test_score_spikes_far_above_the_rest(dev, ws, g):
+    """Keys whose scores exceed every other score by ~300 (natural log units):
+    any lane that took a smaller reference maximum than its row's would form
+    probabilities near 2^400 and overflow.  Positive queries and keys of 32.0
+    in every dim place spikes at keys 5, 13 and 389 only (key % 8 in 4..7,
+    which the upper half of a wavefront holds in the prefill score layout, so
+    a row maximum taken over the lower half alone misses them)."""
+    shape = wl.AttnShape(8 * g, 8)
+    seqs = _seqs(shape, [(128, 512), (1, 300), (1, 77)], seed=21 + g)
+    spike = np.uint16(0x4200)  # bf16 32.0
+    for s in seqs:
+        q = s.stream.q
+        q &= np.uint16(0x7FFF)  # every query positive
+        for key in (5, 13, 389):
+            if key < s.kv_len:
+                s.stream.k[key] = spike
+    it = rt.Iteration(D.make_dims(8 * g, 8), seqs, _pool_for(seqs), 801, dev,
+                      fill_bits=rt.BF16_NAN_BITS)
+    out = it.run(ws, SCALE, torch.float32)
+    torch.cuda.synchronize()
+    assert D.dlfp_workspace_error(ws.buf) == 0
+    _compare(_to64(out), seqs, f"score spikes g={g}")
