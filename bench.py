@@ -186,9 +186,8 @@ class Sweep:
         ct, vp = self.ct, self.ct.c_void_p
         dims_ref, stream = self.dims_ref, self.stream_handle
         app_args = (dims_ref, T, vp(k.data_ptr()), vp(v.data_ptr()), vp(st.d_slots.data_ptr()))
-        att_head = (dims_ref, ct.byref(meta.c), vp(st.d_cu_q.data_ptr()),
-                    vp(st.d_kv_len.data_ptr()), vp(st.d_q_pos0.data_ptr()),
-                    vp(st.d_work.data_ptr()), vp(d_bt.data_ptr()), int(bt.shape[1]),
+        att_head = (dims_ref, ct.byref(meta.c), vp(st.d_work.data_ptr()), vp(d_bt.data_ptr()),
+                    int(bt.shape[1]),
                     self.num_blocks, vp(q.data_ptr()))
         att_tail = (self.c_scale, vp(self.out.data_ptr()), 0, vp(ws.data_ptr()),
                     ct.c_size_t(ws.numel()), stream)
@@ -428,42 +427,50 @@ def run_extra(name, dev, log_fn):
 
 def run_replays(dev, seeds, log_fn):
     """Closed-loop replay (100 Poisson arrivals at 2 req/s, prompts U[256,4096],
-    128 output tokens, one layer timed, clock x28): paired uncapped baseline and
-    DLFP per seed; the target is 1.2x the median decode-only iteration latency of
-    the seed's baseline run."""
+    128 output tokens, one layer timed, clock x28), paired per seed: the uncapped
+    baseline, fixed caps of 2048 / 3072 / 4096 tokens, and DLFP with the target at
+    1.2x the median decode-only iteration latency of the seed's baseline run.
+    Reductions of the P99 inter-token latency against the baseline get a paired
+    Student-t interval over the seeds."""
     from paper_2609_38386_amd import replay as rp
+    keys = ("itl_p50_ms", "itl_p99_ms", "ttft_p50_ms", "ttft_p99_ms", "e2e_p99_ms",
+            "iterations", "guarded_iterations", "guarded_L_over_T_mean", "controlled_iterations",
+            "controlled_L_over_T_mean", "controlled_within_target", "reconciled")
+    policies = ["fixed_2048", "fixed_3072", "fixed_4096", "dlfp"]
     out = {"per_seed": {}}
-    reductions = []
+    reductions = {k: [] for k in policies}
     for seed in seeds:
         cfg = rp.ReplayConfig(seed=seed)
         ex = rp.GpuExecutor(cfg, dev)
         trace = []
         t0 = time.time()
-        base = rp.run_replay(cfg, rp.Policy(rp.Policy.UNCAPPED), ex, trace=trace)
+        runs = {"uncapped": rp.run_replay(cfg, rp.Policy(rp.Policy.UNCAPPED), ex, trace=trace)}
         dec = [it["layer_ms"] for it in trace if it["decoders"] > 0 and it["p_t"] == 0]
         target = 1.2 * float(np.median(dec))
-        trace_d = []
-        dl = rp.run_replay(cfg, rp.Policy(rp.Policy.DLFP, target_ms=target, cfg=cfg), ex,
-                           trace=trace_d)
-        red = 100.0 * (base["itl_p99_ms"] - dl["itl_p99_ms"]) / base["itl_p99_ms"]
-        reductions.append(red)
-        keys = ("itl_p50_ms", "itl_p99_ms", "ttft_p50_ms", "ttft_p99_ms", "e2e_p99_ms",
-                "iterations", "guarded_iterations", "guarded_L_over_T_mean", "reconciled")
-        out["per_seed"][str(seed)] = {
-            "target_layer_ms": round(target, 5),
-            "baseline": {k: (round(base[k], 4) if isinstance(base[k], float) else base[k])
-                         for k in keys},
-            "dlfp": {k: (round(dl[k], 4) if isinstance(dl[k], float) else dl[k]) for k in keys},
-            "p99_itl_reduction_pct": round(red, 2),
-        }
-        log_fn(f"replay seed {seed}: {time.time() - t0:.1f}s, p99 ITL {base['itl_p99_ms']:.3f} -> "
-               f"{dl['itl_p99_ms']:.3f} ms, guarded {dl['guarded_iterations']}")
+        for cap in (2048, 3072, 4096):
+            runs[f"fixed_{cap}"] = rp.run_replay(cfg, rp.Policy(rp.Policy.FIXED, cap=cap), ex)
+        runs["dlfp"] = rp.run_replay(cfg, rp.Policy(rp.Policy.DLFP, target_ms=target, cfg=cfg), ex)
+        base = runs["uncapped"]
+        rec = {"target_layer_ms": round(target, 5)}
+        for name, r in runs.items():
+            rec[name] = {k: (round(r[k], 4) if isinstance(r[k], float) else r[k]) for k in keys}
+            if name in reductions:
+                red = 100.0 * (base["itl_p99_ms"] - r["itl_p99_ms"]) / base["itl_p99_ms"]
+                rec[name]["p99_itl_reduction_pct"] = round(red, 2)
+                reductions[name].append(red)
+        out["per_seed"][str(seed)] = rec
+        log_fn(f"replay seed {seed}: {time.time() - t0:.1f}s, p99 ITL uncapped "
+               f"{base['itl_p99_ms']:.3f} ms, dlfp {runs['dlfp']['itl_p99_ms']:.3f} ms, "
+               f"guarded {runs['dlfp']['guarded_iterations']}")
         del ex
-    mean, lo, hi = rp.paired_ci(reductions)
-    out["p99_itl_reduction_mean_pct"] = round(mean, 2)
-    out["p99_itl_reduction_ci95_pct"] = None if lo is None else [round(lo, 2), round(hi, 2)]
-    out["note"] = ("latencies are x28 one-layer device times; at 2 req/s requests rarely "
-                   "overlap, so few iterations are guarded")
+    out["p99_itl_reduction_vs_uncapped"] = {}
+    for name, reds in reductions.items():
+        mean, lo, hi = rp.paired_ci(reds)
+        out["p99_itl_reduction_vs_uncapped"][name] = {
+            "mean_pct": round(mean, 2),
+            "ci95_pct": None if lo is None else [round(lo, 2), round(hi, 2)]}
+    out["note"] = ("latencies are x28 one-layer device times (attention only); at 2 req/s "
+                   "requests rarely overlap, so few iterations are guarded")
     return out
 
 

@@ -100,10 +100,13 @@ typedef struct {
 
 /* How the attention launch splits key ranges (split-K).  Zero fields pick
  * the built-in policy: prefill key ranges are cut so the prefill share offers
- * about one unit per compute unit (never below 1024 keys), decode
- * ranges into sqrt(256 W / F) keys for W decode keys over the F resident
- * wavefronts the prefill units leave free, and a range longer than its split
- * is cut into equal parts. */
+ * about one unit per compute unit (never below 1024 keys); a prefill share
+ * too small to offer that many units is latency-bound and takes tiles of 32
+ * rows (32 / g tokens) with the shortest of 256, 512 or 1024-key splits that
+ * keeps its units within two per compute unit; decode ranges are cut into
+ * sqrt(256 W / F) keys for W decode keys over the F resident wavefronts the
+ * prefill units leave free; a range longer than its split is cut into equal
+ * parts. */
 typedef struct {
   int32_t decode_split_tokens;   /* keys per decode unit; 0 = auto, else a multiple of 16,
                                     at most DLFP_MAX_DECODE_UNIT_KEYS */
@@ -112,6 +115,8 @@ typedef struct {
   int32_t target_units;          /* wavefronts the device keeps resident for the attention
                                     launch, which the automatic split sizes are fitted to;
                                     0 = DLFP_DEFAULT_RESIDENT_WAVES */
+  int32_t prefill_tile_tokens;   /* prompt tokens per prefill unit; 0 = auto, else at most
+                                    DLFP_TILE_ROWS / g */
 } dlfp_tuning;
 
 /* 256 compute units x 8 resident wavefronts (two 256-thread workgroups per CU). */
@@ -150,7 +155,10 @@ enum {
                           slot holds O (rows x 128 floats), m[rows], l[rows] (rows = tokens x g),
                           padded to a multiple of 64 floats */
   DLFP_W_WSGROUP = 10, /* float offset of the group's split 0 partial */
-  DLFP_W_KIND = 11     /* DLFP_KIND_PREFILL or DLFP_KIND_DECODE */
+  DLFP_W_KIND = 11,    /* DLFP_KIND_PREFILL or DLFP_KIND_DECODE */
+  DLFP_W_QROW0 = 12,   /* packed row of the unit's first token in q and out:
+                          cu_q[seq] + QTOK0 */
+  DLFP_W_QPOS0 = 13    /* position of the unit's first token: q_pos0[seq] + QTOK0 */
 };
 enum { DLFP_KIND_PREFILL = 0, DLFP_KIND_DECODE = 1 };
 
@@ -165,7 +173,7 @@ enum { DLFP_KIND_PREFILL = 0, DLFP_KIND_DECODE = 1 };
  *   cu_q[s]   = sum_{r<s} q_len[r];   q_pos0[s] = kv_len[s] - q_len[s]
  *   slot_mapping[cu_q[s] + i] = block_table[s][p / 16] * 16 + p % 16, p = q_pos0[s] + i
  *   work: prefill units (sequences with q_len > 1) first, one per
- *   (sequence, KV head, tile of DLFP_TILE_ROWS / g tokens, key split); then
+ *   (sequence, KV head, tile of at most DLFP_TILE_ROWS / g tokens, key split); then
  *   decode units (q_len == 1), one per (sequence, KV head, key split).
  *   Splits of the same rows form a group whose partial results the attention
  *   launch combines in split order.
@@ -192,9 +200,9 @@ int dlfp_kv_append(const dlfp_dims* dims, int32_t num_tokens, const void* k_new,
  * KV head h / g:  out = softmax_j(scale * q.k_j) v_j over keys j <= p.
  *
  * meta: the host metadata from dlfp_build_varlen_meta (only its counts are
- * read).  d_cu_q, d_kv_len, d_q_pos0, d_work, d_block_table: device copies of
- * meta->cu_q, the kv_len given to the builder, meta->q_pos0, meta->work and
- * the block table.  q, k_cache, v_cache: device bf16.  out: device,
+ * read).  d_work, d_block_table: device copies of meta->work (each record
+ * carries its sequence, rows, positions and key range) and of the block
+ * table.  q, k_cache, v_cache: device bf16.  out: device,
  * out_dtype 0 = bf16, 1 = fp32.  workspace: device scratch of at least
  * meta->workspace_bytes whose header and counter region (the first
  * DLFP_WORKSPACE_PARTIALS bytes) were zeroed once by dlfp_workspace_init;
@@ -203,8 +211,7 @@ int dlfp_kv_append(const dlfp_dims* dims, int32_t num_tokens, const void* k_new,
  * Errors: DLFP_EINVAL, DLFP_ENOSPC (workspace too small), DLFP_EUNSUPPORTED,
  * DLFP_EHIP.  A block id outside [0, num_blocks) met on the device is not
  * read; the launch raises the workspace error word instead (dlfp_workspace_error). */
-int dlfp_attention_mixed(const dlfp_dims* dims, const dlfp_meta* meta, const int32_t* d_cu_q,
-                         const int32_t* d_kv_len, const int32_t* d_q_pos0, const int32_t* d_work,
+int dlfp_attention_mixed(const dlfp_dims* dims, const dlfp_meta* meta, const int32_t* d_work,
                          const int32_t* d_block_table, int32_t max_blocks, int32_t num_blocks,
                          const void* q, const void* k_cache, const void* v_cache, float scale,
                          void* out, int32_t out_dtype, void* workspace, size_t workspace_bytes,

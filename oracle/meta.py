@@ -30,6 +30,7 @@ WS_MAX_GROUPS = 65536    # fixed counter region: one int32 per possible group
 # Work-item field indices (16 int32 per unit).
 W_SEQ, W_KVHEAD, W_QTOK0, W_QNTOK, W_KVBEGIN, W_KVEND = 0, 1, 2, 3, 4, 5
 W_GROUP, W_SPLIT, W_NSPLITS, W_WSOFF, W_WSGROUP, W_KIND = 6, 7, 8, 9, 10, 11
+W_QROW0, W_QPOS0 = 12, 13   # derived: cu_q[seq] + first token, q_pos0[seq] + first token
 WORK_INTS = 16
 KIND_PREFILL, KIND_DECODE = 0, 1
 
@@ -63,7 +64,8 @@ def check_work_list(work: np.ndarray, num_prefill: int, q_len: Sequence[int],
     is covered by exactly one unit; units respect sequence bounds and page
     alignment; prefill units precede decode units; a unit is a decode unit iff
     its sequence has a single new token; split groups are complete and ordered;
-    partial-result slots are disjoint and inside the workspace.
+    partial-result slots are disjoint and inside the workspace; the derived
+    row and position fields equal their definitions.
     """
     def fail(msg):
         raise WorkListError(msg)
@@ -78,6 +80,7 @@ def check_work_list(work: np.ndarray, num_prefill: int, q_len: Sequence[int],
         fail("more groups than counters")
     partial_base = (WS_HEADER + 4 * WS_MAX_GROUPS) // 4
     slots = []
+    cu_q = np.concatenate([[0], np.cumsum(np.asarray(q_len, dtype=np.int64))])
     for u, it in enumerate(work):
         s, kh, t0, nt, kb, ke = (int(x) for x in it[:6])
         grp, split, nsp, wsoff, wsgrp, kind = (int(x) for x in it[6:12])
@@ -91,6 +94,8 @@ def check_work_list(work: np.ndarray, num_prefill: int, q_len: Sequence[int],
             fail(f"unit {u}: key range [{kb},{ke}) invalid for kv_len {kl}")
         if ke > pos0 + t0 + nt:
             fail(f"unit {u}: keys beyond the last row's position")
+        if int(it[W_QROW0]) != int(cu_q[s]) + t0 or int(it[W_QPOS0]) != pos0 + t0:
+            fail(f"unit {u}: derived row/position fields")
         want_kind = KIND_DECODE if ql == 1 else KIND_PREFILL
         if kind != want_kind:
             fail(f"unit {u}: kind {kind} but q_len {ql}")

@@ -71,9 +71,6 @@ constexpr float LOG2E = 1.4426950408889634f;
 static_assert(4 * DEC_WAVE_LDS <= LDS_BYTES, "decode slices must fit the shared buffer");
 
 struct Args {
-  const int32_t* cu_q;
-  const int32_t* kv_len;
-  const int32_t* q_pos0;
   const int32_t* work;
   const int32_t* block_table;
   const uint16_t* q;
@@ -323,6 +320,73 @@ __device__ __forceinline__ u32x4_t mask_elems(u32x4_t v, int limit, F key_of) {
   return v;
 }
 
+// Last arriver's merge of a prefill group: every split's (O, m, l) in split
+// order with an online rescale.  TPR threads per row; a row's 128 values are
+// 32 four-float pieces (chunk c = piece / 2, half = piece % 2 of the partial
+// layout), and the thread with index sub in its row takes pieces
+// sub + TPR i.  The loads of NB splits (pieces, maxima and sums) are issued
+// before any is consumed, so a batch costs about one memory round trip; NB is
+// chosen so that a batch holds about 136 registers.  Every load instruction
+// of a wavefront reads whole contiguous runs of the partial layout.
+template <int G, int TPR>
+__device__ __forceinline__ void prefill_merge(const Args& a, const Slots sl, int slot_floats,
+                                              int nsplits, int rows, int row0, int kh) {
+  constexpr int NP = 32 / TPR;             // pieces per thread
+  constexpr int PP = NP < 8 ? NP : 8;      // pieces per pass
+  constexpr int PASSES = NP / PP;
+  constexpr int NB = 32 / PP;              // splits per batch
+  const int tid = threadIdx.x;
+  if (tid >= TPR * rows) return;
+  const int row = tid / TPR, sub = tid % TPR;
+  const int64_t orow = ((int64_t)(row0 + row / G) * a.hq + kh * G + row % G) * D;
+  for (int pass = 0; pass < PASSES; ++pass) {
+    float M = NEG_BIG, lsum = 0.f;
+    f32x4_t acc[PP];
+#pragma unroll
+    for (int i = 0; i < PP; ++i) acc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < nsplits; j += NB) {
+      float mj[NB], lj[NB];
+      f32x4_t x[NB][PP];
+#pragma unroll
+      for (int u = 0; u < NB; ++u) {
+        const int b = min(j + u, nsplits - 1) * slot_floats;
+        mj[u] = pload1(sl, b + rows * D + row);
+        lj[u] = pload1(sl, b + rows * D + rows + row);
+#pragma unroll
+        for (int i = 0; i < PP; ++i) {
+          const int piece = sub + TPR * (pass * PP + i);
+          x[u][i] = pload4(sl, b + (((piece >> 1) * rows + row) * 8 + 4 * (piece & 1)));
+        }
+      }
+      float mn = M;
+#pragma unroll
+      for (int u = 0; u < NB; ++u)
+        if (j + u < nsplits) mn = fmaxf(mn, mj[u]);
+      const float rs = fexp2(M - mn);
+      M = mn;
+      lsum *= rs;
+#pragma unroll
+      for (int i = 0; i < PP; ++i) acc[i] *= rs;
+#pragma unroll
+      for (int u = 0; u < NB; ++u) {
+        const float w = j + u < nsplits ? fexp2(mj[u] - mn) : 0.f;
+        lsum += w * lj[u];
+#pragma unroll
+        for (int i = 0; i < PP; ++i) acc[i] += w * x[u][i];
+      }
+    }
+    const float inv = 1.f / lsum;
+#pragma unroll
+    for (int i = 0; i < PP; ++i) {
+      // piece -> chunk c = 4 mb + g4 and half h -> dims 32 mb + 8 g4 + 4 h
+      const int piece = sub + TPR * (pass * PP + i);
+      const int c = piece >> 1;
+      const int dim = 32 * (c >> 2) + 8 * (c & 3) + 4 * (piece & 1);
+      store4(a, orow + dim, acc[i][0] * inv, acc[i][1] * inv, acc[i][2] * inv, acc[i][3] * inv);
+    }
+  }
+}
+
 template <int G>
 __device__ void prefill_unit(const Args& a, const int32_t* it, char* smem, int* flag) {
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -331,7 +395,8 @@ __device__ void prefill_unit(const Args& a, const int32_t* it, char* smem, int* 
   const int t0 = it[DLFP_W_QTOK0], nt = it[DLFP_W_QNTOK];
   const int kb = it[DLFP_W_KVBEGIN], ke = it[DLFP_W_KVEND];
   const int nsplits = it[DLFP_W_NSPLITS];
-  const int q0 = a.cu_q[s], pos0 = a.q_pos0[s];
+  // First packed row and first position of the sequence's new tokens.
+  const int q0 = it[DLFP_W_QROW0] - t0, pos0 = it[DLFP_W_QPOS0] - t0;
   const int32_t* bt = a.block_table + (int64_t)s * a.max_blocks;
 
   const int r = wave * 32 + col;       // this lane's row within the tile
@@ -626,57 +691,14 @@ __device__ void prefill_unit(const Args& a, const int32_t* it, char* smem, int* 
   __syncthreads();
   if (!*flag) return;
 
-  // Last arriver: merge every split of the group in split order with an
-  // online rescale.  Two threads per row (thread t: row t / 2, half t % 2) and
-  // two passes over the 16 chunks of O; the loads of four splits are issued
-  // before any is consumed, so a pass costs about one memory round trip per
-  // four splits, and every load instruction reads a contiguous kilobyte.
-  if (tid < 2 * rows) {
-    const int row = tid >> 1, h = tid & 1;
-    const int trow = row / G, hrow = row % G;
-    const int64_t orow = ((int64_t)(q0 + t0 + trow) * a.hq + kh * G + hrow) * D;
-    for (int pass = 0; pass < 2; ++pass) {
-      float M = NEG_BIG, lsum = 0.f;
-      f32x4_t acc[8];
-#pragma unroll
-      for (int i = 0; i < 8; ++i) acc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-      for (int j = 0; j < nsplits; j += 4) {
-        float mj[4], lj[4];
-        f32x4_t x[4][8];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int b = min(j + u, nsplits - 1) * slot_floats;
-          mj[u] = pload1(sl, b + rows * D + row);
-          lj[u] = pload1(sl, b + rows * D + rows + row);
-#pragma unroll
-          for (int i = 0; i < 8; ++i) x[u][i] = pload4(sl, b + ((8 * pass + i) * rows + row) * 8 + 4 * h);
-        }
-        float mn = M;
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-          if (j + u < nsplits) mn = fmaxf(mn, mj[u]);
-        const float rs = fexp2(M - mn);
-        M = mn;
-        lsum *= rs;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) acc[i] *= rs;
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const float w = j + u < nsplits ? fexp2(mj[u] - mn) : 0.f;
-          lsum += w * lj[u];
-#pragma unroll
-          for (int i = 0; i < 8; ++i) acc[i] += w * x[u][i];
-        }
-      }
-      const float inv = 1.f / lsum;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {  // chunk 8 pass + i: mb = 2 pass + i / 4, g4 = i % 4
-        const int dim = 32 * (2 * pass + (i >> 2)) + 8 * (i & 3) + 4 * h;
-        store4(a, orow + dim, acc[i][0] * inv, acc[i][1] * inv, acc[i][2] * inv,
-               acc[i][3] * inv);
-      }
-    }
-  }
+  // Last arriver: merge every split of the group (threads per row chosen so
+  // that the whole workgroup takes part).
+  if (rows > 64)
+    prefill_merge<G, 2>(a, sl, slot_floats, nsplits, rows, q0 + t0, kh);
+  else if (rows > 32)
+    prefill_merge<G, 4>(a, sl, slot_floats, nsplits, rows, q0 + t0, kh);
+  else
+    prefill_merge<G, 8>(a, sl, slot_floats, nsplits, rows, q0 + t0, kh);
   if (tid == 0)
     __hip_atomic_store(group_counter(a.ws, grp), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -693,7 +715,7 @@ __device__ void decode_unit(const Args& a, const int32_t* it, char* wl) {
   const int s = uniform(it[DLFP_W_SEQ]), kh = uniform(it[DLFP_W_KVHEAD]);
   const int kb = uniform(it[DLFP_W_KVBEGIN]), ke = uniform(it[DLFP_W_KVEND]);
   const int nsplits = uniform(it[DLFP_W_NSPLITS]);
-  const int tok = uniform(a.cu_q[s]);
+  const int tok = uniform(it[DLFP_W_QROW0]);
   const int32_t* bt = a.block_table + (int64_t)s * a.max_blocks;
   char* kl = wl;
   char* vl = wl + PAGE_ELEMS * 2;
@@ -899,50 +921,69 @@ __device__ void decode_unit(const Args& a, const int32_t* it, char* wl) {
   old = __shfl(old, 0);
   if (old != nsplits - 1) return;
 
-  // Last arriver.  Entry f = j G + h stands for head h of split j.  Lanes
-  // first load the entries' maxima (64 at a time) and reduce them per head
-  // (lane l keeps the maximum of head l % G), then load the entries' row sums
-  // and weights, and accumulate the partial outputs in split order, sixteen
-  // entries' loads issued together.
+  // Last arriver.  Entry f = j G + h stands for head h of split j.  Per batch
+  // of up to 64 entries, lane e loads entry e's maximum and row sum while
+  // every lane loads its two dims of the batch's entries (in groups of 16,
+  // only as many groups as the batch has entries), so a batch costs one
+  // memory round trip; the running per-head maximum rescales what earlier
+  // batches summed, and entries are accumulated in split order.
   const int nf = nsplits * G;
-  float mlane = NEG_BIG;
-  for (int f0 = 0; f0 < nf; f0 += 64) {
-    const int f = f0 + lane;
-    if (f < nf) mlane = fmaxf(mlane, pload1(sl, (f / G) * slot_floats + G * D + f % G));
+  float M[G], lsum[G], acc0[G], acc1[G];
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    M[h] = NEG_BIG;
+    lsum[h] = acc0[h] = acc1[h] = 0.f;
   }
-#pragma unroll
-  for (int sh = G; sh < 64; sh <<= 1) mlane = fmaxf(mlane, shfl_xor(mlane, sh));
-  float lsum[G], acc0[G], acc1[G];
-#pragma unroll
-  for (int h = 0; h < G; ++h) lsum[h] = acc0[h] = acc1[h] = 0.f;
   for (int f0 = 0; f0 < nf; f0 += 64) {
-    const int f = f0 + lane;
-    float wf = 0.f, lf = 0.f;
-    if (f < nf) {
-      const int base = (f / G) * slot_floats + G * D;
-      wf = fexp2(pload1(sl, base + f % G) - mlane);
-      lf = pload1(sl, base + G + f % G);
-    }
     const int n = min(64, nf - f0);
-    for (int e0 = 0; e0 < n; e0 += 16) {
-      f32x2_t v[16];
+    const int fl = f0 + min(lane, n - 1);
+    const int lbase = (fl / G) * slot_floats + G * D + fl % G;
+    const float mf = lane < n ? pload1(sl, lbase) : NEG_BIG;
+    const float lf = pload1(sl, lbase + G);
+    f32x2_t v[4][16];
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int fe = f0 + min(e0 + e, n - 1);
-        v[e] = pload2(sl, (fe / G) * slot_floats + (fe % G) * D + 2 * lane);
+    for (int q = 0; q < 4; ++q) {
+      if (16 * q < n) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int fe = f0 + min(16 * q + e, n - 1);
+          v[q][e] = pload2(sl, (fe / G) * slot_floats + (fe % G) * D + 2 * lane);
+        }
       }
+    }
+    // Batch maximum of head lane % G (f0 is a multiple of 64, so entry
+    // f0 + e belongs to head e % G).
+    float bm = mf;
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int src = min(e0 + e, n - 1);
-        const bool ok = e0 + e < n;
-        const float w = ok ? __builtin_bit_cast(float, __builtin_amdgcn_readlane(
-                                                           __builtin_bit_cast(int, wf), src))
-                           : 0.f;
-        const float lw = __builtin_bit_cast(
-            float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, lf), src));
-        lsum[e % G] += w * lw;
-        acc0[e % G] += w * v[e][0];
-        acc1[e % G] += w * v[e][1];
+    for (int sh = G; sh < 64; sh <<= 1) bm = fmaxf(bm, shfl_xor(bm, sh));
+    float mh = NEG_BIG;
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      const float mnew = fmaxf(M[h], __builtin_bit_cast(float, __builtin_amdgcn_readlane(
+                                                                  __builtin_bit_cast(int, bm), h)));
+      const float rs = fexp2(M[h] - mnew);
+      M[h] = mnew;
+      lsum[h] *= rs;
+      acc0[h] *= rs;
+      acc1[h] *= rs;
+      if (lane % G == h) mh = mnew;
+    }
+    const float wf = lane < n ? fexp2(mf - mh) : 0.f;
+    const float wl = wf * lf;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if (16 * q < n) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int src = 16 * q + e;  // weights of entries past the batch are zero
+          const float w = __builtin_bit_cast(float, __builtin_amdgcn_readlane(
+                                                        __builtin_bit_cast(int, wf), src));
+          const float lw = __builtin_bit_cast(float, __builtin_amdgcn_readlane(
+                                                         __builtin_bit_cast(int, wl), src));
+          lsum[e % G] += lw;
+          acc0[e % G] += w * v[q][e][0];
+          acc1[e % G] += w * v[q][e][1];
+        }
       }
     }
   }
@@ -1031,8 +1072,7 @@ hipError_t launch(const Args& a, int grid, hipStream_t stream) {
 }  // namespace
 
 extern "C" int dlfp_attention_mixed(const dlfp_dims* dims, const dlfp_meta* meta,
-                                    const int32_t* d_cu_q, const int32_t* d_kv_len,
-                                    const int32_t* d_q_pos0, const int32_t* d_work,
+                                    const int32_t* d_work,
                                     const int32_t* d_block_table, int32_t max_blocks,
                                     int32_t num_blocks, const void* q, const void* k_cache,
                                     const void* v_cache, float scale, void* out,
@@ -1048,8 +1088,7 @@ extern "C" int dlfp_attention_mixed(const dlfp_dims* dims, const dlfp_meta* meta
       meta->num_prefill_units > meta->num_units || meta->num_groups < 0)
     return DLFP_EINVAL;
   if (meta->num_units == 0) return DLFP_OK;
-  if (!d_cu_q || !d_kv_len || !d_q_pos0 || !d_work || !d_block_table || !q || !k_cache ||
-      !v_cache || !out || !workspace)
+  if (!d_work || !d_block_table || !q || !k_cache || !v_cache || !out || !workspace)
     return DLFP_EINVAL;
   if (max_blocks <= 0 || num_blocks <= 0) return DLFP_EINVAL;
   if ((int64_t)workspace_bytes < meta->workspace_bytes ||
@@ -1057,9 +1096,6 @@ extern "C" int dlfp_attention_mixed(const dlfp_dims* dims, const dlfp_meta* meta
     return DLFP_ENOSPC;
   if (meta->num_groups > DLFP_MAX_GROUPS) return DLFP_EINVAL;
   Args a;
-  a.cu_q = d_cu_q;
-  a.kv_len = d_kv_len;
-  a.q_pos0 = d_q_pos0;
   a.work = d_work;
   a.block_table = d_block_table;
   a.q = static_cast<const uint16_t*>(q);

@@ -80,7 +80,7 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
   if (!meta || num_seqs < 0) return DLFP_EINVAL;
   if (num_seqs > 0 && (!q_len || !kv_len || !block_table || max_blocks <= 0)) return DLFP_EINVAL;
   if (num_blocks < 0) return DLFP_EINVAL;
-  dlfp_tuning tn = {0, 0, 0};
+  dlfp_tuning tn = {0, 0, 0, 0};
   if (tuning) tn = *tuning;
   if (tn.decode_split_tokens < 0 || tn.decode_split_tokens % DLFP_PAGE_SIZE ||
       tn.decode_split_tokens > DLFP_MAX_DECODE_UNIT_KEYS)
@@ -89,9 +89,11 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
       tn.prefill_split_tokens > DLFP_MAX_PREFILL_UNIT_KEYS)
     return DLFP_EINVAL;
   if (tn.target_units < 0) return DLFP_EINVAL;
+  if (tn.prefill_tile_tokens < 0 || tn.prefill_tile_tokens > DLFP_TILE_ROWS / g)
+    return DLFP_EINVAL;
   const int64_t resident = tn.target_units ? tn.target_units : DLFP_DEFAULT_RESIDENT_WAVES;
   const int hkv = dims->num_kv_heads;
-  const int tile_tokens = DLFP_TILE_ROWS / g;
+  int tile_tokens = tn.prefill_tile_tokens ? tn.prefill_tile_tokens : DLFP_TILE_ROWS / g;
 
   // Validate sequences and the pages they use.
   int64_t tokens = 0, pre_keys = 0;
@@ -116,11 +118,51 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
   }
   if (tokens > std::numeric_limits<int32_t>::max()) return DLFP_ERANGE;
 
+  // Prefill units of the iteration for a tile size and key split.
+  auto prefill_units = [&](int64_t tt, int64_t split) {
+    int64_t n = 0;
+    for (int s = 0; s < num_seqs; ++s) {
+      if (q_len[s] == 1) continue;
+      const int64_t pos0 = kv_len[s] - q_len[s];
+      for (int64_t t0 = 0; t0 < q_len[s]; t0 += tt)
+        n += hkv * ceil_div(pos0 + t0 + std::min<int64_t>(tt, q_len[s] - t0), split);
+    }
+    return n;
+  };
   // Prefill split: long key ranges are cut so that the prefill share offers
   // about one unit per compute unit (eight resident wavefronts; two prefill
   // workgroups sharing a CU each run at little more than half speed), never
-  // below 1024 keys.
+  // below 1024 keys.  A launch too small to give every CU a workgroup that
+  // way (decode units counted four to a workgroup, at the split they would
+  // take without prefill) is bound by the latency of its longest unit and of
+  // the merge of its splits: its prefill takes tiles of 32 rows (a merge then
+  // moves a quarter of the bytes) and the shortest split of 256, 512 or 1024
+  // keys that keeps all workgroups within the two a CU holds.
   int64_t split_p = tn.prefill_split_tokens;
+  int64_t dec_keys = 0, dec_wgs0 = 0;
+  for (int s = 0; s < num_seqs; ++s)
+    if (q_len[s] == 1) dec_keys += (int64_t)kv_len[s] * hkv;
+  if (dec_keys > 0) {
+    const int64_t sd0 = std::clamp<int64_t>(
+        round_up((int64_t)std::ceil(std::sqrt(256.0 * (double)dec_keys / (double)resident)),
+                 DLFP_PAGE_SIZE),
+        128, DLFP_MAX_DECODE_UNIT_KEYS);
+    int64_t du = 0;
+    for (int s = 0; s < num_seqs; ++s)
+      if (q_len[s] == 1) du += hkv * ceil_div(kv_len[s], sd0);
+    dec_wgs0 = ceil_div(du, 4);
+  }
+  if (!split_p && !tn.prefill_tile_tokens && pre_keys > 0 &&
+      prefill_units(tile_tokens, 1024) + dec_wgs0 < resident / 8) {
+    const int small = std::max(1, 32 / g);
+    for (int64_t sp : {256, 512, 1024}) {
+      if (prefill_units(small, sp) + dec_wgs0 <= resident / 4) {
+        tile_tokens = small;
+        split_p = sp;
+        break;
+      }
+    }
+  }
   if (!split_p)
     split_p = std::clamp<int64_t>(
         round_up(std::max<int64_t>(1, ceil_div(pre_keys, std::max<int64_t>(1, resident / 8))), 64),
@@ -133,12 +175,9 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
   // workgroup holds four; at least half stay free).
   int64_t split_d = tn.decode_split_tokens;
   if (!split_d) {
-    int64_t pre_units = 0, dec_keys = 0;
+    int64_t pre_units = 0;
     for (int s = 0; s < num_seqs; ++s) {
-      if (q_len[s] == 1) {
-        dec_keys += (int64_t)kv_len[s] * hkv;
-        continue;
-      }
+      if (q_len[s] == 1) continue;
       const int64_t pos0 = kv_len[s] - q_len[s];
       for (int64_t t0 = 0; t0 < q_len[s]; t0 += tile_tokens) {
         const int64_t nt = std::min<int64_t>(tile_tokens, q_len[s] - t0);
@@ -153,6 +192,8 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
 
   // Build units: prefill (KV-head-major), then decode.
   std::vector<Unit> units;
+  std::vector<int64_t> cu_q_of(num_seqs + 1, 0);  // packed row of each sequence's first token
+  for (int s = 0; s < num_seqs; ++s) cu_q_of[s + 1] = cu_q_of[s] + q_len[s];
   int32_t groups = 0;
   std::vector<int64_t> group_rows;  // rows of each group
   // A key range longer than the split is cut into equal parts (rounded up
@@ -177,6 +218,8 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
       u.f[DLFP_W_SPLIT] = (int32_t)j;
       u.f[DLFP_W_NSPLITS] = (int32_t)nsp;
       u.f[DLFP_W_KIND] = kind;
+      u.f[DLFP_W_QROW0] = (int32_t)(cu_q_of[s] + t0);
+      u.f[DLFP_W_QPOS0] = (int32_t)(kv_len[s] - q_len[s] + t0);
       units.push_back(u);
     }
   };

@@ -43,7 +43,7 @@ class dlfp_dims(ctypes.Structure):
 
 class dlfp_tuning(ctypes.Structure):
     _fields_ = [("decode_split_tokens", ctypes.c_int32), ("prefill_split_tokens", ctypes.c_int32),
-                ("target_units", ctypes.c_int32)]
+                ("target_units", ctypes.c_int32), ("prefill_tile_tokens", ctypes.c_int32)]
 
 
 _P32 = ctypes.POINTER(ctypes.c_int32)
@@ -91,7 +91,7 @@ def lib():
                                          ctypes.POINTER(dlfp_meta)]
     L.dlfp_kv_append.argtypes = [ctypes.POINTER(dlfp_dims), i32, vp, vp, vp, vp, vp, i32, vp]
     L.dlfp_attention_mixed.argtypes = [ctypes.POINTER(dlfp_dims), ctypes.POINTER(dlfp_meta),
-                                       vp, vp, vp, vp, vp, i32, i32, vp, vp, vp, ctypes.c_float,
+                                       vp, vp, i32, i32, vp, vp, vp, ctypes.c_float,
                                        vp, i32, vp, sz, vp]
     L.dlfp_workspace_init.argtypes = [vp, sz, vp]
     L.dlfp_workspace_error.argtypes = [vp, _P32, vp]
@@ -199,15 +199,14 @@ def dlfp_kv_append(dims: dlfp_dims, k_new, v_new, slot_mapping, k_cache, v_cache
     _check(st, "dlfp_kv_append")
 
 
-def dlfp_attention_mixed(dims: dlfp_dims, meta: Meta, d_cu_q, d_kv_len, d_q_pos0, d_work,
-                         d_block_table, q, k_cache, v_cache, scale: float, out, workspace,
-                         stream=None) -> None:
+def dlfp_attention_mixed(dims: dlfp_dims, meta: Meta, d_work, d_block_table, q, k_cache,
+                         v_cache, scale: float, out, workspace, stream=None) -> None:
     """out dtype selects the output precision (bfloat16 or float32)."""
     import torch
     out_dtype = {torch.bfloat16: 0, torch.float32: 1}[out.dtype]
     st = lib().dlfp_attention_mixed(
-        ctypes.byref(dims), ctypes.byref(meta.c), _dptr(d_cu_q), _dptr(d_kv_len),
-        _dptr(d_q_pos0), _dptr(d_work), _dptr(d_block_table), int(d_block_table.shape[1]),
+        ctypes.byref(dims), ctypes.byref(meta.c), _dptr(d_work), _dptr(d_block_table),
+        int(d_block_table.shape[1]),
         int(k_cache.shape[0]), _dptr(q), _dptr(k_cache), _dptr(v_cache), float(scale),
         _dptr(out), out_dtype, _dptr(workspace), int(workspace.numel() * workspace.element_size()),
         _stream(stream))

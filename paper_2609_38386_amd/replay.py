@@ -125,6 +125,9 @@ class Policy:
             self.ctrl = D.dlfp_controller_init(target_ms, cfg.c_initial, cfg.c_min, cfg.c_max,
                                                cfg.quantum)
         self.next_cap = -1 if kind != self.FIXED else cap
+        # True when the next cycle's cap comes from a feedback update (Eq. 2)
+        # rather than from c_initial after a reset.
+        self.controlled = False
 
     def limit(self, n_decoding: int, budget: int) -> int:
         if n_decoding == 0 or self.kind == self.UNCAPPED:
@@ -136,6 +139,10 @@ class Policy:
 
     def observe(self, n_decoding_next: int, guarded: bool, observed_ms: float):
         if self.kind == self.DLFP:
+            if guarded:
+                self.controlled = True
+            elif n_decoding_next == 0:
+                self.controlled = False
             self.next_cap = self._D.dlfp_controller_step(self.ctrl, n_decoding_next, guarded,
                                                          observed_ms)
 
@@ -158,6 +165,7 @@ def run_replay(cfg: ReplayConfig, policy: Policy, execute: Executor,
     active: List[Request] = []   # arrived and not finished, in arrival order
     iterations = guarded_n = 0
     guarded_ratio = []
+    controlled_ratio = []   # guarded cycles whose cap came from a feedback update
     while nxt < len(reqs) or active:
         if not active:
             clock = max(clock, reqs[nxt].arrival_s)
@@ -192,6 +200,7 @@ def run_replay(cfg: ReplayConfig, policy: Policy, execute: Executor,
         bt = np.full((len(rows), cfg.max_blocks), -1, dtype=np.int32)
         for i, pages in enumerate(rows):
             bt[i, :len(pages)] = pages
+        controlled = policy.controlled
         ms = float(execute(np.asarray(q_len, np.int32), np.asarray(kv_len, np.int32), bt))
         iter_ms = cfg.layers * ms
         clock += iter_ms * 1e-3
@@ -214,6 +223,8 @@ def run_replay(cfg: ReplayConfig, policy: Policy, execute: Executor,
             guarded_n += 1
             if policy.target_ms:
                 guarded_ratio.append(ms / policy.target_ms)
+                if controlled:
+                    controlled_ratio.append(ms / policy.target_ms)
         policy.observe(n_next, guarded, ms)
         if trace is not None:
             trace.append({"t": round(clock, 6), "decoders": len(decoders), "p_t": p_t,
@@ -233,6 +244,10 @@ def run_replay(cfg: ReplayConfig, policy: Policy, execute: Executor,
         "ttft_p99_ms": float(np.percentile(ttft, 99)),
         "e2e_p99_ms": float(np.percentile(e2e, 99)),
         "guarded_L_over_T_mean": float(np.mean(guarded_ratio)) if guarded_ratio else None,
+        "controlled_iterations": len(controlled_ratio),
+        "controlled_L_over_T_mean": float(np.mean(controlled_ratio)) if controlled_ratio else None,
+        "controlled_within_target": (float(np.mean(np.asarray(controlled_ratio) <= 1.0))
+                                     if controlled_ratio else None),
         "reconciled": reconciled,
         "prompt_tokens": int(sum(r.prompt_len for r in reqs)),
         "output_tokens": int(sum(r.generated for r in reqs)),
@@ -289,7 +304,7 @@ class GpuExecutor:
         self.ws = rt.Workspace(device, 64 << 20)
         self.timer = D.Timer()
         self.scale = 1.0 / math.sqrt(128)
-        self.hold_us = 300
+        self.hold_us = 150
 
     def __call__(self, q_len: np.ndarray, kv_len: np.ndarray, bt: np.ndarray) -> float:
         D = self.D
@@ -305,9 +320,8 @@ class GpuExecutor:
         D.dlfp_stream_hold(self.hold_us)
         self.timer.start()
         D.dlfp_kv_append(self.dims, self.k[:T], self.v[:T], st.d_slots, self.pool.k, self.pool.v)
-        D.dlfp_attention_mixed(self.dims, st.meta, st.d_cu_q, st.d_kv_len, st.d_q_pos0, st.d_work,
-                               d_bt, self.q[:T], self.pool.k, self.pool.v, self.scale,
-                               self.out[:T], ws)
+        D.dlfp_attention_mixed(self.dims, st.meta, st.d_work, d_bt, self.q[:T], self.pool.k,
+                               self.pool.v, self.scale, self.out[:T], ws)
         self.timer.stop()
         return self.timer.elapsed_ms()
 

@@ -76,17 +76,11 @@ class Batch:
         self.meta = _d.dlfp_build_varlen_meta(dims, self.q_len, self.kv_len, block_table,
                                               num_blocks, tuning)
         m = self.meta
-        n = m.num_seqs
         self.num_tokens = m.num_tokens
-        host = np.concatenate([m.cu_q[:n + 1], self.kv_len[:n], m.q_pos0[:n],
-                               m.slot_mapping[:m.num_tokens], m.work.reshape(-1)]).astype(np.int32)
+        host = np.concatenate([m.slot_mapping[:m.num_tokens], m.work.reshape(-1)]).astype(np.int32)
         dev = torch.from_numpy(host).to(device)
-        o = 0
-        self.d_cu_q = dev[o:o + n + 1]; o += n + 1
-        self.d_kv_len = dev[o:o + n]; o += n
-        self.d_q_pos0 = dev[o:o + n]; o += n
-        self.d_slots = dev[o:o + m.num_tokens]; o += m.num_tokens
-        self.d_work = dev[o:]
+        self.d_slots = dev[:m.num_tokens]
+        self.d_work = dev[m.num_tokens:]
         if d_block_table is None:
             d_block_table = torch.from_numpy(np.ascontiguousarray(block_table, dtype=np.int32)
                                              ).to(device)
@@ -98,9 +92,8 @@ class Batch:
     def attention(self, pool: KVPool, q: torch.Tensor, scale: float, out: torch.Tensor,
                   workspace: Workspace, stream=None):
         ws = workspace.ensure(self.meta.workspace_bytes, self.meta.num_groups, stream)
-        _d.dlfp_attention_mixed(self.dims, self.meta, self.d_cu_q, self.d_kv_len,
-                                self.d_q_pos0, self.d_work, self.d_block_table, q, pool.k,
-                                pool.v, scale, out, ws, stream)
+        _d.dlfp_attention_mixed(self.dims, self.meta, self.d_work, self.d_block_table, q,
+                                pool.k, pool.v, scale, out, ws, stream)
 
 
 class Iteration:
@@ -166,7 +159,7 @@ class StagedBatch:
         self.dims = dims
         self.tuning = tuning if tuning is not None else _d.dlfp_tuning(0, 0, 0)
         self.meta = _d.Meta(cap_seqs, cap_tokens, cap_work)
-        total = (cap_seqs + 1) + 2 * cap_seqs + cap_tokens + cap_work * _d.WORK_INTS
+        total = cap_tokens + cap_work * _d.WORK_INTS
         self.host = torch.empty(total, dtype=torch.int32, pin_memory=True)
         self.host_np = self.host.numpy()
         self.dev = torch.empty(total, dtype=torch.int32, device=device)
@@ -181,20 +174,16 @@ class StagedBatch:
             _d._ptr32(kv_len), _d._ptr32(block_table), block_table.shape[1], int(num_blocks),
             ct.byref(m.c))
         _d._check(st, "dlfp_build_varlen_meta")
-        n, T, U = m.c.num_seqs, m.c.num_tokens, m.c.num_units
+        T, U = m.c.num_tokens, m.c.num_units
         h = self.host_np
         o = 0
         offs = []
-        for arr, cnt in ((m.cu_q, n + 1), (kv_len, n), (m.q_pos0, n), (m.slot_mapping, T),
-                         (m.work_buf.reshape(-1), U * _d.WORK_INTS)):
+        for arr, cnt in ((m.slot_mapping, T), (m.work_buf.reshape(-1), U * _d.WORK_INTS)):
             h[o:o + cnt] = arr[:cnt]
             offs.append((o, cnt))
             o += cnt
         self.dev[:o].copy_(self.host[:o], non_blocking=True)
-        (a, na), (b, nb), (c, nc), (d, nd), (e, ne) = offs
-        self.d_cu_q = self.dev[a:a + na]
-        self.d_kv_len = self.dev[b:b + nb]
-        self.d_q_pos0 = self.dev[c:c + nc]
+        (d, nd), (e, ne) = offs
         self.d_slots = self.dev[d:d + nd]
         self.d_work = self.dev[e:e + ne]
         self.num_tokens = T

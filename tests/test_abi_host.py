@@ -55,10 +55,14 @@ def test_meta_tiny_iteration():
     rows = np.concatenate([bt[4:5], bt[:4]])
     dims = D.make_dims(16, 8)
     _check_against_twin(dims, q_len, kv_len, rows, cfg.pool_size())
-    for tn in [D.dlfp_tuning(16, 64, 0), D.dlfp_tuning(32, 128, 0), D.dlfp_tuning(0, 0, 64)]:
+    for tn in [D.dlfp_tuning(16, 64, 0), D.dlfp_tuning(32, 128, 0), D.dlfp_tuning(0, 0, 64),
+               D.dlfp_tuning(0, 64, 0, 8)]:
         meta = _check_against_twin(dims, q_len, kv_len, rows, cfg.pool_size(), tn)
         if tn.decode_split_tokens == 16:
             assert meta.num_groups > 0
+        if tn.prefill_tile_tokens == 8:   # 128 prompt tokens in tiles of 8, per KV head
+            pre = meta.work[:meta.num_prefill_units]
+            assert (pre[:, 3] <= 8).all() and len(np.unique(pre[:, 2])) == 16
 
 
 @pytest.mark.parametrize("p,chunk", [(64, 0), (256, 17), (2048, 3)])
@@ -90,8 +94,29 @@ def test_meta_random_mixes(seed):
     pages = [wl.pages_for(k) for k in kv_len]
     pool = sum(pages) + 5
     bt = wl.block_tables(seed, pages, pool, max_blocks=max(pages) + 2)
-    tn = D.dlfp_tuning(int(rng.choice([0, 16, 48, 128])), int(rng.choice([0, 64, 192])), 0)
+    tn = D.dlfp_tuning(int(rng.choice([0, 16, 48, 128])), int(rng.choice([0, 64, 192])), 0,
+                       int(rng.integers(0, 128 // g + 1)))
     _check_against_twin(D.make_dims(g * hkv, hkv), q_len, kv_len, bt, pool, tn)
+
+
+def test_meta_small_prefill_share_takes_latency_tiles():
+    # a 32-token chunk over a 3000-token prefix next to one decoder (g = 2):
+    # too few units at full tiles, so 16-token tiles and 256-key splits
+    dims = D.make_dims(16, 8)
+    q_len, kv_len = [32, 1], [3032, 2000]
+    bt = np.arange(2 * 190, dtype=np.int32).reshape(2, 190)
+    meta = _check_against_twin(dims, q_len, kv_len, bt, 2 * 190)
+    pre = meta.work[:meta.num_prefill_units]
+    assert meta.prefill_split_tokens == 256
+    assert pre[:, 3].max() == 16 and len(pre) == 2 * 8 * 12
+    # a 2048-token chunk fills the device at full tiles: throughput policy
+    cfg = wl.qwen3_0_6b_config()
+    bt6 = wl.block_tables(cfg.seed, cfg.pages_per_seq(), cfg.pool_size())
+    its = cfg.iteration(2048, 3)
+    meta = _check_against_twin(dims, [q for _, q, _ in its], [k for _, _, k in its],
+                               bt6[[x for x, _, _ in its]], cfg.pool_size())
+    assert meta.prefill_split_tokens >= 1024
+    assert meta.work[:meta.num_prefill_units, 3].max() == 64
 
 
 def test_meta_empty_batch():
@@ -121,6 +146,9 @@ def test_meta_errors():
         assert e.value.status == -5
     with pytest.raises(D.DlfpError) as e:
         D.dlfp_build_varlen_meta(dims, [1], [5], bt, 4, D.dlfp_tuning(10, 0, 0))
+    assert e.value.status == -1
+    with pytest.raises(D.DlfpError) as e:           # g = 2: at most 64 tokens per tile
+        D.dlfp_build_varlen_meta(dims, [1], [5], bt, 4, D.dlfp_tuning(0, 0, 0, 65))
     assert e.value.status == -1
 
 

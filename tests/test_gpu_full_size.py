@@ -66,8 +66,8 @@ class FullSize:
         q.normal_(generator=self.gen)
         out = torch.empty((T, self.hq, 128), dtype=torch.float32, device=self.dev)
         ws = self.ws.ensure(st.meta.workspace_bytes)
-        D.dlfp_attention_mixed(self.dims, st.meta, st.d_cu_q, st.d_kv_len, st.d_q_pos0, st.d_work,
-                               d_bt, q, self.pool.k, self.pool.v, SCALE, out, ws)
+        D.dlfp_attention_mixed(self.dims, st.meta, st.d_work, d_bt, q, self.pool.k, self.pool.v,
+                               SCALE, out, ws)
         torch.cuda.synchronize()
         assert D.dlfp_workspace_error(ws) == 0
         self.check(its, q, out, bt)

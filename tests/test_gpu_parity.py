@@ -157,6 +157,25 @@ def test_gqa_groups_ragged(dev, ws, g, hkv):
     _compare(_to64(out), seqs, f"g={g} hkv={hkv}")
 
 
+@pytest.mark.parametrize("split,tile", [(64, 0), (192, 0), (256, 16), (320, 0), (1024, 8),
+                                        (512, 1), (0, 0)])
+def test_prefill_splits_and_small_tiles(dev, ws, split, tile):
+    """Key ranges of 1, 3, 4, 5 and up to 16 tiles with ragged ends; tiles of
+    fewer tokens than a full one (down to a single token)."""
+    shape = wl.AttnShape(16, 8)
+    specs = [(37, 1111), (100, 700), (1, 900), (64, 333), (5, 1029), (1, 70)]
+    seqs = _seqs(shape, specs, seed=31 + split + tile)
+    it = rt.Iteration(D.make_dims(16, 8), seqs, _pool_for(seqs), 6, dev,
+                      fill_bits=rt.BF16_NAN_BITS,
+                      tuning=D.dlfp_tuning(64, split, 0, tile))
+    out = it.run(ws, SCALE, torch.float32)
+    torch.cuda.synchronize()
+    assert D.dlfp_workspace_error(ws.buf) == 0
+    _compare(_to64(out), seqs, f"split={split} tile={tile}")
+    hdr = ws.buf[:D.WORKSPACE_PARTIALS].view(torch.int32).cpu().numpy()
+    assert not hdr.any()
+
+
 def test_decode_only_and_prefill_only(dev, ws):
     shape = wl.AttnShape(16, 8)
     dec = _seqs(shape, [(1, n) for n in (64, 100, 256, 511, 1000)], seed=11)
@@ -209,17 +228,16 @@ def test_abi_rejects_bad_arguments(dev, ws):
     small = torch.empty(D.WORKSPACE_PARTIALS - 4, dtype=torch.uint8, device=dev)
     b = it.batch
     with pytest.raises(D.DlfpError) as e:
-        D.dlfp_attention_mixed(b.dims, b.meta, b.d_cu_q, b.d_kv_len, b.d_q_pos0, b.d_work,
-                               b.d_block_table, it.q, it.pool.k, it.pool.v, SCALE, out, small)
+        D.dlfp_attention_mixed(b.dims, b.meta, b.d_work, b.d_block_table, it.q, it.pool.k,
+                               it.pool.v, SCALE, out, small)
     assert e.value.status == -3
     with pytest.raises(D.DlfpError) as e:
-        D.dlfp_attention_mixed(b.dims, b.meta, b.d_cu_q, b.d_kv_len, b.d_q_pos0, b.d_work,
-                               b.d_block_table, it.q, it.pool.k, it.pool.v, -1.0, out, ws.buf)
+        D.dlfp_attention_mixed(b.dims, b.meta, b.d_work, b.d_block_table, it.q, it.pool.k,
+                               it.pool.v, -1.0, out, ws.buf)
     assert e.value.status == -1
     with pytest.raises(D.DlfpError) as e:
-        D.dlfp_attention_mixed(D.make_dims(16, 8, head_dim=64), b.meta, b.d_cu_q, b.d_kv_len,
-                               b.d_q_pos0, b.d_work, b.d_block_table, it.q, it.pool.k, it.pool.v,
-                               SCALE, out, ws.buf)
+        D.dlfp_attention_mixed(D.make_dims(16, 8, head_dim=64), b.meta, b.d_work,
+                               b.d_block_table, it.q, it.pool.k, it.pool.v, SCALE, out, ws.buf)
     assert e.value.status == -5
 
 

@@ -41,9 +41,14 @@ def test_slots_unique_and_owned():
             assert slots[t] % 16 == pos % 16
 
 
+# the hand-built list below: q_len [70, 1], kv_len [100, 40]
+_CU_Q, _POS0 = [0, 70], [30, 39]
+
+
 def _unit(seq, kh, t0, nt, kb, ke, grp=-1, split=0, nsp=1, wsoff=0, wsgrp=0, kind=0):
     u = np.zeros(om.WORK_INTS, dtype=np.int32)
-    u[:12] = [seq, kh, t0, nt, kb, ke, grp, split, nsp, wsoff, wsgrp, kind]
+    u[:14] = [seq, kh, t0, nt, kb, ke, grp, split, nsp, wsoff, wsgrp, kind,
+              _CU_Q[seq] + t0, _POS0[seq] + t0]
     return u
 
 
@@ -74,7 +79,8 @@ def test_checker_accepts_valid_list():
 
 
 @pytest.mark.parametrize("defect", ["drop", "overlap", "order", "kind", "gap", "slot",
-                                    "rows", "beyond", "align", "splitidx", "ws"])
+                                    "rows", "beyond", "align", "splitidx", "ws", "qrow",
+                                    "qpos"])
 def test_checker_rejects_planted_defects(defect):
     work, npre, ql, kl, hq, hkv, ng, ws = _valid_list()
     work = work.copy()
@@ -102,5 +108,9 @@ def test_checker_rejects_planted_defects(defect):
         work[1, om.W_SPLIT] = 0
     elif defect == "ws":
         ws = 100
+    elif defect == "qrow":
+        work[2, om.W_QROW0] += 1
+    elif defect == "qpos":
+        work[3, om.W_QPOS0] -= 1
     with pytest.raises(om.WorkListError):
         om.check_work_list(work, npre, ql, kl, hq, hkv, ng, ws)

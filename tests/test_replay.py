@@ -89,3 +89,19 @@ def test_fixed_cap_policy():
 def test_paired_ci_matches_student_t():
     mean, lo, hi = rp.paired_ci([24.767, 30.053, 28.209])
     assert abs(mean - 27.68) < 0.01 and abs(lo - 21.01) < 0.02 and abs(hi - 34.34) < 0.02
+
+
+def test_controlled_cycles_hold_a_reachable_target():
+    """Once a feedback update has set the cap (Eq. 2), guarded cycles sit at the
+    target when the smallest chunk can meet it; the first cycle of an episode
+    runs at c_initial and is reported apart."""
+    cfg = _cfg(n_requests=12, rate_per_s=200.0, out_len=64)
+    model = rp.linear_latency_model(0.01, 1e-5, 1e-4)
+    r = rp.run_replay(cfg, rp.Policy(rp.Policy.DLFP, target_ms=0.03, cfg=cfg), model)
+    assert r["controlled_iterations"] > 0
+    assert r["controlled_iterations"] < r["guarded_iterations"]
+    assert 0.8 <= r["controlled_L_over_T_mean"] <= 1.1
+    assert r["controlled_within_target"] >= 0.5
+    assert r["guarded_L_over_T_mean"] >= r["controlled_L_over_T_mean"]
+    base = rp.run_replay(cfg, rp.Policy(rp.Policy.UNCAPPED), model)
+    assert base["controlled_iterations"] == 0 and base["controlled_L_over_T_mean"] is None
