@@ -118,6 +118,58 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
   }
   if (tokens > std::numeric_limits<int32_t>::max()) return DLFP_ERANGE;
 
+  // Decode split for F free wavefronts.  The launch time is roughly the share
+  // of work per resident wavefront plus the longest unit, and every unit adds
+  // a fixed cost (query and block-table loads, pipeline fill, its part of the
+  // merge) worth about 256 keys; the split minimising the sum is
+  // sqrt(256 W / F) keys for W decode keys.  When that split needs no more
+  // units than F (one round, no queue), the launch instead lasts as long as
+  // the busiest CU, ceil(workgroups / CUs) units of the longest length: a
+  // split leaving some CUs two workgroups and others one wastes half of the
+  // latter, so among the splits that keep to one round (multiples of 16 keys
+  // from 128 up, in steps of about 6%) the one minimising that estimate is
+  // taken, ties going to the longer.
+  int32_t max_kv = 0;
+  int64_t dec_keys = 0;
+  for (int s = 0; s < num_seqs; ++s)
+    if (q_len[s] == 1) {
+      max_kv = std::max(max_kv, kv_len[s]);
+      dec_keys += (int64_t)kv_len[s] * hkv;
+    }
+  auto decode_split = [&](int64_t free_waves) -> int64_t {
+    free_waves = std::max<int64_t>(8, free_waves);
+    const double root = std::sqrt(256.0 * (double)dec_keys / (double)free_waves);
+    const int64_t s0 = std::clamp<int64_t>(round_up((int64_t)std::ceil(root), DLFP_PAGE_SIZE), 128,
+                                           DLFP_MAX_DECODE_UNIT_KEYS);
+    auto units_and_longest = [&](int64_t sp, int64_t* longest) {
+      int64_t n_units = 0;
+      *longest = 0;
+      for (int s = 0; s < num_seqs; ++s) {
+        if (q_len[s] != 1) continue;
+        const int64_t n = ceil_div(kv_len[s], sp);
+        n_units += hkv * n;
+        *longest = std::max(*longest, round_up(ceil_div(kv_len[s], n), DLFP_PAGE_SIZE));
+      }
+      return n_units;
+    };
+    int64_t longest = 0;
+    if (units_and_longest(s0, &longest) > free_waves) return s0;
+    const int64_t free_cus = free_waves / 8;
+    int64_t best_sp = s0;
+    double best = std::numeric_limits<double>::infinity();
+    const int64_t top = std::min<int64_t>(round_up(std::max<int32_t>(max_kv, 128), DLFP_PAGE_SIZE),
+                                          DLFP_MAX_DECODE_UNIT_KEYS);
+    for (int64_t sp = 128; sp <= top; sp = round_up(sp + std::max<int64_t>(16, sp / 16), 16)) {
+      const int64_t n_units = units_and_longest(sp, &longest);
+      if (n_units > free_waves) continue;
+      const double e = (double)ceil_div(ceil_div(n_units, 4), free_cus) * (double)(longest + 256);
+      if (e <= best) {
+        best = e;
+        best_sp = sp;
+      }
+    }
+    return best_sp;
+  };
   // Prefill units of the iteration for a tile size and key split.
   auto prefill_units = [&](int64_t tt, int64_t split) {
     int64_t n = 0;
@@ -139,18 +191,12 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
   // moves a quarter of the bytes) and the shortest split of 256, 512 or 1024
   // keys that keeps all workgroups within the two a CU holds.
   int64_t split_p = tn.prefill_split_tokens;
-  int64_t dec_keys = 0, dec_wgs0 = 0;
-  for (int s = 0; s < num_seqs; ++s)
-    if (q_len[s] == 1) dec_keys += (int64_t)kv_len[s] * hkv;
-  if (dec_keys > 0) {
-    const int64_t sd0 = std::clamp<int64_t>(
-        round_up((int64_t)std::ceil(std::sqrt(256.0 * (double)dec_keys / (double)resident)),
-                 DLFP_PAGE_SIZE),
-        128, DLFP_MAX_DECODE_UNIT_KEYS);
-    int64_t du = 0;
+  int64_t dec_wgs0 = 0;
+  {
+    const int64_t sd0 = tn.decode_split_tokens ? tn.decode_split_tokens : decode_split(resident);
     for (int s = 0; s < num_seqs; ++s)
-      if (q_len[s] == 1) du += hkv * ceil_div(kv_len[s], sd0);
-    dec_wgs0 = ceil_div(du, 4);
+      if (q_len[s] == 1) dec_wgs0 += hkv * ceil_div(kv_len[s], sd0);
+    dec_wgs0 = ceil_div(dec_wgs0, 4);
   }
   if (!split_p && !tn.prefill_tile_tokens && pre_keys > 0 &&
       prefill_units(tile_tokens, 1024) + dec_wgs0 < resident / 8) {
@@ -167,12 +213,6 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
     split_p = std::clamp<int64_t>(
         round_up(std::max<int64_t>(1, ceil_div(pre_keys, std::max<int64_t>(1, resident / 8))), 64),
         1024, DLFP_MAX_PREFILL_UNIT_KEYS);
-  // Decode split.  The launch time is roughly the share of work per resident
-  // wavefront plus the longest unit, and every unit adds a fixed cost (query
-  // and block-table loads, pipeline fill, its part of the merge) worth about
-  // 256 keys; the split minimising the sum is sqrt(256 W / F) keys for W
-  // decode keys over the F wavefronts the prefill units leave free (a prefill
-  // workgroup holds four; at least half stay free).
   int64_t split_d = tn.decode_split_tokens;
   if (!split_d) {
     int64_t pre_units = 0;
@@ -184,10 +224,7 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
         pre_units += hkv * ceil_div(pos0 + t0 + nt, split_p);
       }
     }
-    const int64_t free_waves = resident - 4 * std::min(pre_units, resident / 8);
-    const double best = std::sqrt(256.0 * (double)dec_keys / (double)std::max<int64_t>(1, free_waves));
-    split_d = std::clamp<int64_t>(round_up((int64_t)std::ceil(best), DLFP_PAGE_SIZE), 128,
-                                  DLFP_MAX_DECODE_UNIT_KEYS);
+    split_d = decode_split(resident - 4 * std::min(pre_units, resident / 8));
   }
 
   // Build units: prefill (KV-head-major), then decode.
