@@ -103,11 +103,12 @@ typedef struct {
  * about one unit per compute unit (never below 1024 keys); a prefill share
  * too small to offer that many units is latency-bound and takes tiles of 32
  * rows (32 / g tokens) with the shortest of 256, 512 or 1024-key splits that
- * keeps its units within two per compute unit; decode ranges are cut into
- * sqrt(256 W / F) keys for W decode keys over the F resident wavefronts the
- * prefill units leave free, unless that needs no more units than F, where the
- * split keeping to one round that best evens the workgroups over the CUs is
- * taken; a range longer than its split is cut into equal parts. */
+ * keeps its units within two per compute unit; the decode split is either
+ * sqrt(256 W / F) keys for W decode keys over the F wavefronts of the
+ * workgroup slots the prefill units leave (several queue rounds), or the
+ * split that fits one round and best evens the decode workgroups over the
+ * CUs, whichever an estimate of the launch time favours; a range longer than
+ * its split is cut into equal parts. */
 typedef struct {
   int32_t decode_split_tokens;   /* keys per decode unit; 0 = auto, else a multiple of 16,
                                     at most DLFP_MAX_DECODE_UNIT_KEYS */

@@ -86,6 +86,7 @@ struct Args {
   int32_t num_prefill;
   int32_t out_f32;
   int32_t decode_waves;  // wavefronts of the decode workgroups of this launch
+  int32_t decode_static; // decode units handed out by position, the rest by queue
   float scale_log2;      // softmax scale * log2(e)
 };
 
@@ -1007,26 +1008,32 @@ __global__ __launch_bounds__(THREADS, 2) void attention_mixed_kernel(Args a) {
     const int u = xcd_remap(b, a.num_prefill);
     prefill_unit<G>(a, a.work + (int64_t)u * DLFP_WORK_INTS, smem, &flag);
   } else {
-    // Decode wavefront w of decode workgroup d starts with unit 4 d + w; when
-    // there are more units than wavefronts, the rest form a queue that
-    // wavefronts drain one ticket at a time as they finish, so none idles while
-    // units remain (a workgroup's slot frees only when all four of its
-    // wavefronts are done).  The last workgroup to finish resets the header
-    // words for the next launch.
+    // Decode wavefront w of decode workgroup d starts with unit 4 d + w when
+    // that is one of the first decode_static units (the workgroups resident
+    // from the start); the other units form a queue that wavefronts drain one
+    // ticket at a time as they finish, so none idles while units remain (a
+    // workgroup's slot frees only when all four of its wavefronts are done),
+    // and a workgroup that only becomes resident later takes tickets from the
+    // start instead of holding units back to the tail.  The last workgroup to
+    // finish resets the header words for the next launch.
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     char* wl = smem + wave * DEC_WAVE_LDS;
     const int ndec = a.num_units - a.num_prefill;
-    const bool queue = ndec > a.decode_waves;
+    const bool queue = ndec > a.decode_static;
+    auto ticket = [&]() {
+      int nt = 0;
+      if (lane == 0)
+        nt = a.decode_static + __hip_atomic_fetch_add(header_word(a.ws, HDR_TICKET), 1,
+                                                      __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      return uniform(__shfl(nt, 0));
+    };
     int t = (b - a.num_prefill) * 4 + wave;
+    if (queue && t >= a.decode_static) t = ticket();
     while (t < ndec) {
       decode_unit<G>(a, a.work + (int64_t)(a.num_prefill + t) * DLFP_WORK_INTS, wl);
       wave_sync();
       if (!queue) break;
-      int nt = 0;
-      if (lane == 0)
-        nt = a.decode_waves + __hip_atomic_fetch_add(header_word(a.ws, HDR_TICKET), 1,
-                                                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      t = uniform(__shfl(nt, 0));
+      t = ticket();
     }
     if (queue) {
       __syncthreads();
@@ -1113,9 +1120,15 @@ extern "C" int dlfp_attention_mixed(const dlfp_dims* dims, const dlfp_meta* meta
   a.scale_log2 = scale * LOG2E;
   // Decode workgroups: enough to fill the resident slots of the device (two
   // per CU), fewer when there are fewer units; they drain the decode queue.
+  // Only those that find a slot left by the prefill workgroups from the start
+  // (at least 64) get units by position.
+  const int cus = compute_units();
   const int decode_units = meta->num_units - meta->num_prefill_units;
-  const int decode_wgs = std::min((decode_units + 3) / 4, 2 * compute_units());
+  const int decode_wgs = std::min((decode_units + 3) / 4, 2 * cus);
+  const int slots = meta->num_prefill_units < 2 * cus
+                        ? std::max(2 * cus - meta->num_prefill_units, 64) : 2 * cus;
   a.decode_waves = 4 * decode_wgs;
+  a.decode_static = std::min(decode_units, 4 * std::min(decode_wgs, slots));
   const int grid = meta->num_prefill_units + decode_wgs;
   (void)hipGetLastError();
   hipError_t e;

@@ -118,17 +118,20 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
   }
   if (tokens > std::numeric_limits<int32_t>::max()) return DLFP_ERANGE;
 
-  // Decode split for F free wavefronts.  The launch time is roughly the share
-  // of work per resident wavefront plus the longest unit, and every unit adds
-  // a fixed cost (query and block-table loads, pipeline fill, its part of the
-  // merge) worth about 256 keys; the split minimising the sum is
-  // sqrt(256 W / F) keys for W decode keys.  When that split needs no more
-  // units than F (one round, no queue), the launch instead lasts as long as
-  // the busiest CU, ceil(workgroups / CUs) units of the longest length: a
-  // split leaving some CUs two workgroups and others one wastes half of the
-  // latter, so among the splits that keep to one round (multiples of 16 keys
-  // from 128 up, in steps of about 6%) the one minimising that estimate is
-  // taken, ties going to the longer.
+  // Decode split for `slots` workgroup slots left by the prefill units
+  // (F = 4 slots wavefronts; CUs = resident / 8).  Either the queue runs
+  // several rounds: every unit then adds a fixed cost (query and block-table
+  // loads, pipeline fill, its part of the merge) worth about 256 keys, the
+  // split minimising work / F plus the longest unit is sqrt(256 W / F) keys
+  // for W decode keys, and the launch lasts about units / F unit times plus
+  // one (units of the last round start late and finish alone, slower than
+  // when they shared the device).  Or the units fit in one round (at most F):
+  // the launch then
+  // lasts as long as the busiest CU, ceil(workgroups / min(CUs, slots)) units
+  // of the longest length, so a split leaving some CUs two decode workgroups
+  // and others one wastes half of the latter.  The one-round splits
+  // (multiples of 16 keys from 128 up, in steps of about 6%) are weighed
+  // against the sqrt split by these estimates; ties go to the longer split.
   int32_t max_kv = 0;
   int64_t dec_keys = 0;
   for (int s = 0; s < num_seqs; ++s)
@@ -136,11 +139,10 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
       max_kv = std::max(max_kv, kv_len[s]);
       dec_keys += (int64_t)kv_len[s] * hkv;
     }
-  auto decode_split = [&](int64_t free_waves) -> int64_t {
-    free_waves = std::max<int64_t>(8, free_waves);
-    const double root = std::sqrt(256.0 * (double)dec_keys / (double)free_waves);
-    const int64_t s0 = std::clamp<int64_t>(round_up((int64_t)std::ceil(root), DLFP_PAGE_SIZE), 128,
-                                           DLFP_MAX_DECODE_UNIT_KEYS);
+  auto decode_split = [&](int64_t slots) -> int64_t {
+    slots = std::max<int64_t>(1, slots);
+    const int64_t free_waves = 4 * slots;
+    const int64_t cu_cap = std::max<int64_t>(1, std::min<int64_t>(resident / 8, slots));
     auto units_and_longest = [&](int64_t sp, int64_t* longest) {
       int64_t n_units = 0;
       *longest = 0;
@@ -152,17 +154,21 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
       }
       return n_units;
     };
+    const double root = std::sqrt(256.0 * (double)dec_keys / (double)free_waves);
+    const int64_t s0 = std::clamp<int64_t>(round_up((int64_t)std::ceil(root), DLFP_PAGE_SIZE), 128,
+                                           DLFP_MAX_DECODE_UNIT_KEYS);
     int64_t longest = 0;
-    if (units_and_longest(s0, &longest) > free_waves) return s0;
-    const int64_t free_cus = free_waves / 8;
     int64_t best_sp = s0;
     double best = std::numeric_limits<double>::infinity();
+    const int64_t n0 = units_and_longest(s0, &longest);
+    if (n0 > free_waves)
+      best = ((double)n0 / (double)free_waves + 1.0) * (double)(longest + 256);
     const int64_t top = std::min<int64_t>(round_up(std::max<int32_t>(max_kv, 128), DLFP_PAGE_SIZE),
                                           DLFP_MAX_DECODE_UNIT_KEYS);
     for (int64_t sp = 128; sp <= top; sp = round_up(sp + std::max<int64_t>(16, sp / 16), 16)) {
       const int64_t n_units = units_and_longest(sp, &longest);
       if (n_units > free_waves) continue;
-      const double e = (double)ceil_div(ceil_div(n_units, 4), free_cus) * (double)(longest + 256);
+      const double e = (double)ceil_div(ceil_div(n_units, 4), cu_cap) * (double)(longest + 256);
       if (e <= best) {
         best = e;
         best_sp = sp;
@@ -193,7 +199,7 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
   int64_t split_p = tn.prefill_split_tokens;
   int64_t dec_wgs0 = 0;
   {
-    const int64_t sd0 = tn.decode_split_tokens ? tn.decode_split_tokens : decode_split(resident);
+    const int64_t sd0 = tn.decode_split_tokens ? tn.decode_split_tokens : decode_split(resident / 4);
     for (int s = 0; s < num_seqs; ++s)
       if (q_len[s] == 1) dec_wgs0 += hkv * ceil_div(kv_len[s], sd0);
     dec_wgs0 = ceil_div(dec_wgs0, 4);
@@ -224,7 +230,12 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
         pre_units += hkv * ceil_div(pos0 + t0 + nt, split_p);
       }
     }
-    split_d = decode_split(resident - 4 * std::min(pre_units, resident / 8));
+    // The decode share starts in the workgroup slots (two per CU, four
+    // wavefronts each) that the prefill units leave, at least 64; when the
+    // prefill units take them all, it runs as they retire.
+    split_d = decode_split(pre_units < resident / 4
+                               ? std::max<int64_t>(resident / 4 - pre_units, 64)
+                               : resident / 4);
   }
 
   // Build units: prefill (KV-head-major), then decode.
