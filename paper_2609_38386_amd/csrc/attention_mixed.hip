@@ -759,12 +759,17 @@ __device__ void decode_unit(const Args& a, const int32_t* it, char* wl) {
   }
 
   // NSLOT register buffers rotate: while one page is consumed from LDS the
-  // next NSLOT are in flight (g = 8 keeps one, for registers).  The loop is
+  // next NSLOT are in flight.  One page (8 KiB) per wavefront is enough: the
+  // decode wavefronts of a launch then keep about 8 MB in flight, which
+  // saturates HBM, while more only lengthens the queues that the launch's
+  // prefill units wait in (measured on the Qwen3-0.6B sweep: 48.5-49.7 us per
+  // layer for chunks of 64-256 tokens with one page in flight, 51.9-52.8 us
+  // with two; the decode-only layer is unchanged).  The loop is
   // straight-line: a page index past the unit's last page re-reads that page
   // (an L2 hit) and every key in it is masked, and a block id outside the
   // pool is replaced by block 0 after raising the error word, so the compiler
   // can keep the prefetch in flight.
-  constexpr int NSLOT = G >= 8 ? 1 : 2;
+  constexpr int NSLOT = 1;
   u32x4_t fk[NSLOT][4], fv[NSLOT][4];
   auto fetch = [&](u32x4_t* k4, u32x4_t* v4, int p) {
     const int raw = ptab[min(p, p_end - 1) - p_begin];
