@@ -100,10 +100,14 @@ typedef struct {
 
 /* How the attention launch splits key ranges (split-K).  Zero fields pick
  * the built-in policy: prefill key ranges are cut so the prefill share offers
- * about one unit per compute unit (never below 1024 keys); a prefill share
- * too small to offer that many units is latency-bound and takes tiles of 32
- * rows (32 / g tokens) with the shortest of 256, 512 or 1024-key splits that
- * keeps its units within two per compute unit; the decode split is either
+ * about one unit per compute unit (never below 1024 keys); a launch too
+ * small to offer that many units, even counting its decode workgroups, is
+ * latency-bound and takes tiles of 32 rows (32 / g tokens) with the shortest
+ * of 256, 512 or 1024-key splits that keeps its units within two per compute
+ * unit; otherwise, when the launch has a decode share, the prefill takes the
+ * tallest tile of 128, 64 or 32 rows whose units, at the shortest split of at
+ * least 1024 keys keeping them at most one per compute unit, come within 1/16
+ * of that count (32 rows when none does); the decode split is either
  * sqrt(256 W / F) keys for W decode keys over the F wavefronts of the
  * workgroup slots the prefill units leave (several queue rounds), or the
  * split that fits one round and best evens the decode workgroups over the

@@ -215,6 +215,30 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
       }
     }
   }
+  // Beside a decode share the prefill units wait on loaded memory and their
+  // split merges are on the launch's critical path: the units should number
+  // about one per compute unit (more leave decode workgroups without a slot,
+  // fewer leave long key loops), each as tall as that allows (a shorter tile
+  // re-reads its keys and values more often but merges fewer bytes per row
+  // group).  So the tallest tile of 128, 64 or 32 rows whose units, with the
+  // shortest split of at least 1024 keys that keeps them at most one per
+  // compute unit, come within 1/16 of that count; else 32 rows.  (Measured on
+  // Qwen3-0.6B shapes beside 32 decoders: 44-48 us per layer instead of
+  // 50-54 us for chunks of 64-256 tokens over prefixes of 2-6k keys.)
+  const bool has_decode = dec_keys > 0;
+  if (!split_p && !tn.prefill_tile_tokens && pre_keys > 0 && has_decode) {
+    const int64_t target = std::max<int64_t>(1, resident / 8);
+    for (int rows : {DLFP_TILE_ROWS, DLFP_TILE_ROWS / 2, DLFP_TILE_ROWS / 4}) {
+      const int64_t tt = std::max(1, rows / g);
+      int64_t sp = 1024;
+      while (sp < DLFP_MAX_PREFILL_UNIT_KEYS && prefill_units(tt, sp) > target) sp += 64;
+      if (prefill_units(tt, sp) * 16 >= target * 15 || rows == DLFP_TILE_ROWS / 4) {
+        tile_tokens = (int)tt;
+        split_p = sp;
+        break;
+      }
+    }
+  }
   if (!split_p)
     split_p = std::clamp<int64_t>(
         round_up(std::max<int64_t>(1, ceil_div(pre_keys, std::max<int64_t>(1, resident / 8))), 64),
