@@ -612,6 +612,11 @@ __device__ void prefill_unit(const Args& a, const int32_t* it, char* smem, int* 
       // keeping it unconditional lets the products overlap the exponentials.
       qk(nxt, PAR ^ 1);
       probs(cur, pf);
+      // The PV products and row sums run at raised wave priority: the SIMD
+      // arbiter then keeps feeding the matrix core of the wave that is past
+      // its exponentials while the other waves of the CU finish theirs
+      // (measured 4-7% more prefill throughput on long chunks).
+      __builtin_amdgcn_s_setprio(1);
       pv(pf, PAR);
       rowsum(pf);
       // Issue order: QK(j+1) products interleaved with the exponentials, then
@@ -629,6 +634,7 @@ __device__ void prefill_unit(const Args& a, const int32_t* it, char* smem, int* 
         __builtin_amdgcn_sched_group_barrier(0x002, 1, 0);
         __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
       }
+      __builtin_amdgcn_s_setprio(0);
       if (more) {
         const int k1 = kb + (j + 1) * KV_TILE;
         if (k1 + KV_TILE > wave_lim_min) mask(nxt, k1);
