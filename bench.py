@@ -8,8 +8,10 @@ for every p_t, the prompt is prefilled in 8192 / p_t mixed iterations while
 each decoder advances one token per iteration.  Each iteration is the full hot
 path -- host metadata build and upload, then for each of the 28 layers (28
 distinct KV pools, so KV reads come from HBM rather than the 256 MB Infinity
-Cache) the KV append and the single attention launch, then the completion-
-timed controller step on the iteration's measured device latency.
+Cache) the KV append and the attention, then the completion-
+timed controller step on the iteration's measured device latency.  The KV
+append and the attention run as one launch (dlfp_append_attention_mixed);
+--two-launch times dlfp_kv_append followed by dlfp_attention_mixed instead.
 
 Inputs are seeded synthetic N(0,1) bf16 tensors already resident in HBM; the
 decoders' cached history is written straight into the pools.  Attention
@@ -48,6 +50,9 @@ def parse_args():
     ap.add_argument("--replay-seeds", default="801,802,803",
                     help="seeds of the closed-loop replay (comma list, or 'none')")
     ap.add_argument("--quiet", action="store_true")
+    ap.add_argument("--two-launch", action="store_true",
+                    help="append with dlfp_kv_append, then dlfp_attention_mixed (instead of "
+                         "the one-launch dlfp_append_attention_mixed)")
     ap.add_argument("--pmc-workload", choices=["sweep", "shares"], default=None,
                     help="counter-pass workloads: 'sweep' = one headline sweep plus a 1 GiB "
                          "device copy; 'shares' = decode-only and prefill-only launches")
@@ -84,10 +89,17 @@ def attn_work(hq, hkv, q_len, kv_len):
     return dec_b, pre_b, dec_f, pre_f
 
 
+def append_work(hkv, num_tokens):
+    """Algorithmic bytes of the KV append of one layer: every new token's key and
+    value rows read once and written once into their pages (1024 B per token and
+    KV head at d=128, bf16)."""
+    return num_tokens * hkv * 128 * 2 * 2 * 2
+
+
 # ----------------------------------------------------------------------------- sweep harness
 
 class Sweep:
-    def __init__(self, cfg, dev, n_pools, layers, seed_offset=0):
+    def __init__(self, cfg, dev, n_pools, layers, seed_offset=0, fused=True):
         import torch
         from paper_2609_38386_amd import dlfp as D
         from paper_2609_38386_amd import runtime as rt
@@ -96,6 +108,7 @@ class Sweep:
         self.cfg = cfg
         self.dev = dev
         self.layers = layers
+        self.fused = fused
         sh = cfg.shape
         self.hq, self.hkv = sh.num_q_heads, sh.num_kv_heads
         self.dims = D.make_dims(self.hq, self.hkv)
@@ -177,7 +190,8 @@ class Sweep:
 
     def launch(self, pr, record=True):
         """Enqueue the layers of a prepared iteration between the completion timer's
-        events; with `record`, HIP events also bracket every attention launch."""
+        events; with `record`, HIP events also bracket every attention launch (the
+        one-launch append + attention, or the attention alone with two launches)."""
         D = self.D
         st, T, bt, d_bt = pr["st"], pr["T"], pr["bt"], pr["d_bt"]
         q, k, v = pr["qkv"]
@@ -191,18 +205,26 @@ class Sweep:
                     self.num_blocks, vp(q.data_ptr()))
         att_tail = (self.c_scale, vp(self.out.data_ptr()), 0, vp(ws.data_ptr()),
                     ct.c_size_t(ws.numel()), stream)
+        kv_new = (vp(k.data_ptr()), vp(v.data_ptr()))
         L = self.L
         self.timer.start(self.stream)
         for layer in range(self.layers):
             pk, pv = self.pool_ptrs[layer % len(self.pools)]
-            rc = L.dlfp_kv_append(*app_args, pk, pv, self.num_blocks, stream)
-            if rc:
-                D._check(rc, "dlfp_kv_append")
-            if record:
-                self.ev[layer][0].record(self.stream)
-            rc = L.dlfp_attention_mixed(*att_head, pk, pv, *att_tail)
-            if rc:
-                D._check(rc, "dlfp_attention_mixed")
+            if self.fused:
+                if record:
+                    self.ev[layer][0].record(self.stream)
+                rc = L.dlfp_append_attention_mixed(*att_head, *kv_new, pk, pv, *att_tail)
+                if rc:
+                    D._check(rc, "dlfp_append_attention_mixed")
+            else:
+                rc = L.dlfp_kv_append(*app_args, pk, pv, self.num_blocks, stream)
+                if rc:
+                    D._check(rc, "dlfp_kv_append")
+                if record:
+                    self.ev[layer][0].record(self.stream)
+                rc = L.dlfp_attention_mixed(*att_head, pk, pv, *att_tail)
+                if rc:
+                    D._check(rc, "dlfp_attention_mixed")
             if record:
                 self.ev[layer][1].record(self.stream)
         self.timer.stop(self.stream)
@@ -268,7 +290,7 @@ def run_headline(args, dev, log_fn):
     from paper_2609_38386_amd import workload as wl
     cfg = wl.qwen3_0_6b_config()
     t0 = time.time()
-    sw = Sweep(cfg, dev, n_pools=cfg.layers, layers=cfg.layers)
+    sw = Sweep(cfg, dev, n_pools=cfg.layers, layers=cfg.layers, fused=not args.two_launch)
     log_fn(f"setup {time.time() - t0:.1f}s: {cfg.layers} pools x {sw.num_blocks} blocks")
     # decode-only latency of the first iteration sets the controller target (1.2x)
     dec_ms = [sw.iteration(cfg.chunks[0], 0, prefill=False, record=False)[0] for _ in range(3)]
@@ -300,7 +322,8 @@ def run_headline(args, dev, log_fn):
                 s["recorded"] += 1
                 s["attn_ms"] += sum(attn)
                 db, pb, df, pf = attn_work(sw.hq, sw.hkv, ql, kl)
-                s["bytes"] += (db + pb) * cfg.layers
+                ab = append_work(sw.hkv, int(ql.sum())) if sw.fused else 0
+                s["bytes"] += (db + pb + ab) * cfg.layers
                 s["flops"] += (df + pf) * cfg.layers
 
     for _ in range(args.warmup):
@@ -337,7 +360,8 @@ def run_headline(args, dev, log_fn):
     ach = (bytes_all / n_launch) / avg_launch_s / 1e9
     roofline = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": traffic,
-                "kernel": "attention_mixed_kernel<2>",
+                "kernel": ("attention_mixed_kernel<2, true> (append + attention)" if sw.fused
+                           else "attention_mixed_kernel<2, false>"),
                 "avg_launch_us": round(avg_launch_s * 1e6, 2),
                 "algorithmic_bytes_per_launch": int(bytes_all / n_launch),
                 "algorithmic_tflops": round(flops_all / (attn_ms * 1e-3) / 1e12, 1)}
@@ -357,6 +381,7 @@ def measure_shares(sw, cfg, reps=2):
         _, a, ql, kl = sw.iteration(cfg.chunks[0], r, prefill=False)
         attn += sum(a)
         db, _, df, _ = attn_work(sw.hq, sw.hkv, ql, kl)
+        db += append_work(sw.hkv, int(ql.sum())) if sw.fused else 0
         b += db * sw.layers
         f += df * sw.layers
     gbs = b / (attn * 1e-3) / 1e9
@@ -371,6 +396,7 @@ def measure_shares(sw, cfg, reps=2):
             _, a, ql, kl = sw.iteration(p, c, decoders=False)
             attn += sum(a)
             _, pb, _, pf = attn_work(sw.hq, sw.hkv, ql, kl)
+            pb += append_work(sw.hkv, int(ql.sum())) if sw.fused else 0
             b += pb * sw.layers
             f += pf * sw.layers
         sec = attn * 1e-3
@@ -385,7 +411,7 @@ def measure_shares(sw, cfg, reps=2):
     return out
 
 
-def run_extra(name, dev, log_fn):
+def run_extra(name, dev, log_fn, fused=True):
     """First, middle and last chunk of every p_t for a larger shape."""
     import torch
     from paper_2609_38386_amd import dlfp as D
@@ -393,7 +419,7 @@ def run_extra(name, dev, log_fn):
     cfg = wl.CONFIGS[name]()
     t0 = time.time()
     layers_timed = 2 if cfg.layers > 1 else 1   # each pool far exceeds the 256 MB cache
-    sw = Sweep(cfg, dev, n_pools=layers_timed, layers=layers_timed, seed_offset=1)
+    sw = Sweep(cfg, dev, n_pools=layers_timed, layers=layers_timed, seed_offset=1, fused=fused)
     log_fn(f"{name}: setup {time.time() - t0:.1f}s, {sw.num_blocks} blocks/pool")
     dec_ms = [sw.iteration(cfg.chunks[0], 0, prefill=False)[0] for _ in range(2)]
     ctrl = D.dlfp_controller_init(1.2 * float(np.median(dec_ms)), 2048, 32, 8192, 128)
@@ -406,7 +432,8 @@ def run_extra(name, dev, log_fn):
             ms_l.append(ms / layers_timed)
             attn_l += sum(a)
             db, pb, df, pf = attn_work(sw.hq, sw.hkv, ql, kl)
-            b_l += (db + pb) * layers_timed
+            ab = append_work(sw.hkv, int(ql.sum())) if fused else 0
+            b_l += (db + pb + ab) * layers_timed
             f_l += (df + pf) * layers_timed
         sec = attn_l * 1e-3
         lat[str(p)] = {"iter_ms_per_layer_first_mid_last": [round(x, 4) for x in ms_l],
@@ -512,7 +539,7 @@ def cpu_baseline(seconds):
 
 # ----------------------------------------------------------------------------- main
 
-def pmc_workload(dev, kind):
+def pmc_workload(dev, kind, fused=True):
     """'sweep': one untimed headline sweep, then a plain 1 GiB device-to-device copy
     whose known traffic calibrates the FETCH_SIZE / WRITE_SIZE counters.
     'shares': decode-only launches (28 layers), then prefill-only launches of the
@@ -520,7 +547,7 @@ def pmc_workload(dev, kind):
     import torch
     from paper_2609_38386_amd import workload as wl
     cfg = wl.qwen3_0_6b_config()
-    sw = Sweep(cfg, dev, n_pools=cfg.layers, layers=cfg.layers)
+    sw = Sweep(cfg, dev, n_pools=cfg.layers, layers=cfg.layers, fused=fused)
     if kind == "shares":
         sw.iteration(cfg.chunks[0], 0, prefill=False, record=False)
         sw.iteration(2048, cfg.prompt_len // 2048 - 1, decoders=False, record=False)
@@ -557,7 +584,7 @@ def main():
         sys.exit(1)
     dev = torch.device("cuda:0")
     if args.pmc_workload:
-        pmc_workload(dev, args.pmc_workload)
+        pmc_workload(dev, args.pmc_workload, fused=not args.two_launch)
         return
     logf = lambda *a: log(args, *a)  # noqa: E731
     cfg, r = run_headline(args, dev, logf)
@@ -565,7 +592,7 @@ def main():
     extras = {}
     names = [] if args.configs in ("", "none") else args.configs.split(",")
     for name in names:
-        extras[name] = run_extra(name.strip(), dev, logf)
+        extras[name] = run_extra(name.strip(), dev, logf, fused=not args.two_launch)
         logf(f"{name} done")
     replay = None
     if args.replay_seeds not in ("", "none"):

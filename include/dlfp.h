@@ -14,6 +14,8 @@
  *   dlfp_attention_mixed     device: ONE launch of attention for all rows
  *   dlfp_controller_step     host: Eq. 2 on the completion-timed latency
  *
+ * dlfp_append_attention_mixed does the two device steps in one launch.
+ *
  * The iteration latency that feeds the controller is the completion time of
  * the device work measured with HIP events (dlfp_timer_*), not the interval
  * between scheduler calls -- the proxy the paper identifies as the reason its
@@ -69,8 +71,10 @@ extern "C" {
 #define DLFP_WORK_INTS 16
 /* Workspace layout: a 256-byte header (int32 word 0 = error flag, word
  * DLFP_WORKSPACE_TICKET_WORD = the decode queue's next ticket, word
- * DLFP_WORKSPACE_DONE_WORD = decode workgroups finished; both are zero
- * between launches), then a fixed region of DLFP_MAX_GROUPS int32 split
+ * DLFP_WORKSPACE_DONE_WORD = decode workgroups finished, word
+ * DLFP_WORKSPACE_APPEND_WORD = append workgroups finished, word
+ * DLFP_WORKSPACE_WAITED_WORD = prefill units past their wait for them; all
+ * four are zero between launches), then a fixed region of DLFP_MAX_GROUPS int32 split
  * counters, then partial results from byte DLFP_WORKSPACE_PARTIALS on.  The
  * counter region has the same size for every launch, so one workspace can
  * serve iterations of any shape.  A launch that did not complete (a device
@@ -78,6 +82,8 @@ extern "C" {
 #define DLFP_WORKSPACE_HEADER 256
 #define DLFP_WORKSPACE_TICKET_WORD 16
 #define DLFP_WORKSPACE_DONE_WORD 32
+#define DLFP_WORKSPACE_APPEND_WORD 48
+#define DLFP_WORKSPACE_WAITED_WORD 56
 #define DLFP_MAX_GROUPS 65536
 #define DLFP_WORKSPACE_PARTIALS (DLFP_WORKSPACE_HEADER + 4 * DLFP_MAX_GROUPS)
 
@@ -144,6 +150,8 @@ typedef struct {
   int32_t num_groups;         /* split groups (units sharing output rows) */
   int32_t decode_split_tokens, prefill_split_tokens;  /* splits actually used */
   int64_t workspace_bytes;    /* device workspace the attention launch needs */
+  int32_t num_append;         /* append records stored after the units (see below) */
+  int32_t num_waiting_units;  /* prefill units that read pages the append records write */
 } dlfp_meta;
 
 /* Work unit fields (int32 index into one DLFP_WORK_INTS record). */
@@ -161,12 +169,12 @@ enum {
                           slot holds O (rows x 128 floats), m[rows], l[rows] (rows = tokens x g),
                           padded to a multiple of 64 floats */
   DLFP_W_WSGROUP = 10, /* float offset of the group's split 0 partial */
-  DLFP_W_KIND = 11,    /* DLFP_KIND_PREFILL or DLFP_KIND_DECODE */
+  DLFP_W_KIND = 11,    /* DLFP_KIND_PREFILL, DLFP_KIND_DECODE or DLFP_KIND_APPEND */
   DLFP_W_QROW0 = 12,   /* packed row of the unit's first token in q and out:
                           cu_q[seq] + QTOK0 */
   DLFP_W_QPOS0 = 13    /* position of the unit's first token: q_pos0[seq] + QTOK0 */
 };
-enum { DLFP_KIND_PREFILL = 0, DLFP_KIND_DECODE = 1 };
+enum { DLFP_KIND_PREFILL = 0, DLFP_KIND_DECODE = 1, DLFP_KIND_APPEND = 2 };
 
 /* Build the metadata of one mixed iteration (Eq. 1's D_t and p_t, Sec. 2.1).
  *
@@ -182,11 +190,17 @@ enum { DLFP_KIND_PREFILL = 0, DLFP_KIND_DECODE = 1 };
  *   (sequence, KV head, tile of at most DLFP_TILE_ROWS / g tokens, key split); then
  *   decode units (q_len == 1), one per (sequence, KV head, key split).
  *   Splits of the same rows form a group whose partial results the attention
- *   launch combines in split order.
+ *   launch combines in split order.  After the num_units units follow
+ *   num_append append records (KIND = DLFP_KIND_APPEND), read only by
+ *   dlfp_append_attention_mixed: one per (prompt sequence, KV head, run of its
+ *   new tokens inside one page), with SEQ, KVHEAD, QTOK0, QNTOK (1..16),
+ *   QROW0 and QPOS0 as for units.  num_waiting_units counts the prefill units
+ *   whose last key lies in a page holding a new token of their sequence.
  * Errors: DLFP_EINVAL (null pointers, q_len < 1, kv_len < q_len, bad tuning),
  * DLFP_ERANGE (a used page's block id outside [0, num_blocks) or beyond
  * max_blocks, or more than DLFP_MAX_GROUPS split groups), DLFP_ENOSPC (a capacity in *meta too small; the required counts
- * are still written to num_seqs / num_tokens / num_units), DLFP_EUNSUPPORTED. */
+ * are still written to num_seqs / num_tokens / num_units / num_append; cap_work
+ * must hold num_units + num_append records), DLFP_EUNSUPPORTED. */
 int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int32_t num_seqs,
                            const int32_t* q_len, const int32_t* kv_len,
                            const int32_t* block_table, int32_t max_blocks, int32_t num_blocks,
@@ -223,13 +237,41 @@ int dlfp_attention_mixed(const dlfp_dims* dims, const dlfp_meta* meta, const int
                          void* out, int32_t out_dtype, void* workspace, size_t workspace_bytes,
                          hipStream_t stream);
 
+/* dlfp_kv_append followed by dlfp_attention_mixed, as ONE launch (Sec. 2.1:
+ * the iteration's cache write and its attention).  Arguments as for those two
+ * calls; the slots written are the ones dlfp_build_varlen_meta derives from
+ * the block table (its slot_mapping), d_work must hold the num_append append
+ * records after the units, and k_cache/v_cache are written.  The result (out,
+ * and every cache slot of a new token) equals that of the two calls; slots
+ * that hold no new token are left as they were.
+ *
+ * Inside the launch a decode unit takes its own new key and value from k_new /
+ * v_new and writes them to their slot.  The prompt tokens (the num_append
+ * records) are written by the first workgroups of the grid -- 8 per 64
+ * records; each writes its XCD's L2 back when done -- and count themselves
+ * done on a workspace word; a prefill unit waits for that count, with a bounded poll,
+ * before it loads the first page holding a new token.  The wait cannot hang:
+ * a poll that runs out raises the workspace error word (value 2) and the
+ * launch finishes with undefined output.  The last of the waiting prefill
+ * units to finish zeroes the words again.  When the records would need more
+ * than 16 such workgroups (above 128 records), they are written by a launch
+ * of their own just before, and the prefill units do not wait.
+ * Errors: as dlfp_attention_mixed. */
+int dlfp_append_attention_mixed(const dlfp_dims* dims, const dlfp_meta* meta,
+                                const int32_t* d_work, const int32_t* d_block_table,
+                                int32_t max_blocks, int32_t num_blocks, const void* q,
+                                const void* k_new, const void* v_new, void* k_cache,
+                                void* v_cache, float scale, void* out, int32_t out_dtype,
+                                void* workspace, size_t workspace_bytes, hipStream_t stream);
+
 /* Zero the workspace header and the whole counter region (the first
  * DLFP_WORKSPACE_PARTIALS bytes) with a stream-ordered fill kernel.  Needed
  * once per workspace allocation.  DLFP_ENOSPC if workspace_bytes is smaller. */
 int dlfp_workspace_init(void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* Copy the workspace error word to *host_error after synchronising the stream:
- * 0 = no error, 1 = a block id outside the pool was met. */
+ * 0 = no error, 1 = a block id outside the pool was met, 2 = a prefill unit of
+ * dlfp_append_attention_mixed stopped waiting for the append records. */
 int dlfp_workspace_error(const void* workspace, int32_t* host_error, hipStream_t stream);
 
 /* Proportional prefill-cap controller, Eq. 2 (Sec. 3.1):

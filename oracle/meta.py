@@ -13,7 +13,9 @@ Its metadata has exactly one correct value, written out here with plain loops:
 
 The work list (how the attention launch splits the iteration into units) has
 many valid values, so it is not recomputed; ``check_work_list`` verifies the
-properties any valid list must have.
+properties any valid list must have, and ``check_append_records`` those of the
+records that tell a one-launch append which new tokens to write (each prompt
+token of each KV head exactly once, in runs that stay inside one page).
 """
 from __future__ import annotations
 
@@ -32,7 +34,7 @@ W_SEQ, W_KVHEAD, W_QTOK0, W_QNTOK, W_KVBEGIN, W_KVEND = 0, 1, 2, 3, 4, 5
 W_GROUP, W_SPLIT, W_NSPLITS, W_WSOFF, W_WSGROUP, W_KIND = 6, 7, 8, 9, 10, 11
 W_QROW0, W_QPOS0 = 12, 13   # derived: cu_q[seq] + first token, q_pos0[seq] + first token
 WORK_INTS = 16
-KIND_PREFILL, KIND_DECODE = 0, 1
+KIND_PREFILL, KIND_DECODE, KIND_APPEND = 0, 1, 2
 
 
 def varlen_meta(q_len: Sequence[int], kv_len: Sequence[int], block_table: np.ndarray
@@ -160,3 +162,58 @@ def check_work_list(work: np.ndarray, num_prefill: int, q_len: Sequence[int],
     if WS_HEADER + 4 * WS_MAX_GROUPS > workspace_bytes:
         fail("header and counters exceed the workspace")
     return {"units": len(work), "groups": len(groups)}
+
+
+def check_append_records(records: np.ndarray, work: np.ndarray, num_prefill: int,
+                         q_len: Sequence[int], kv_len: Sequence[int], num_kv_heads: int,
+                         num_waiting: int) -> Dict[str, int]:
+    """Raise ``WorkListError`` unless ``records`` are valid append records.
+
+    Validity: every new token of every prompt sequence (q_len > 1) is covered,
+    per KV head, by exactly one record, and no decoder token is; a record's
+    tokens are consecutive and lie in one page; its derived row and position
+    fields equal their definitions.  ``num_waiting`` must be the number of
+    prefill units whose last key lies in a page at or after the page of their
+    sequence's first new token (the units that read a page holding a new token).
+    """
+    def fail(msg):
+        raise WorkListError(msg)
+
+    n_seq = len(q_len)
+    records = np.asarray(records, dtype=np.int64).reshape(-1, WORK_INTS)
+    cu_q = np.concatenate([[0], np.cumsum(np.asarray(q_len, dtype=np.int64))])
+    cover = {}
+    for r, it in enumerate(records):
+        s, kh, t0, nt = (int(x) for x in it[:4])
+        if int(it[W_KIND]) != KIND_APPEND:
+            fail(f"record {r}: kind {int(it[W_KIND])}")
+        if not (0 <= s < n_seq and 0 <= kh < num_kv_heads):
+            fail(f"record {r}: bad seq/head")
+        ql, kl = int(q_len[s]), int(kv_len[s])
+        if ql == 1:
+            fail(f"record {r}: decoder token (decode units write their own)")
+        pos0 = kl - ql
+        if not (0 <= t0 and 1 <= nt <= PAGE and t0 + nt <= ql):
+            fail(f"record {r}: tokens out of range")
+        if (pos0 + t0) // PAGE != (pos0 + t0 + nt - 1) // PAGE:
+            fail(f"record {r}: run crosses a page")
+        if int(it[W_QROW0]) != int(cu_q[s]) + t0 or int(it[W_QPOS0]) != pos0 + t0:
+            fail(f"record {r}: derived row/position fields")
+        c = cover.setdefault((s, kh), np.zeros(ql, dtype=np.int32))
+        c[t0:t0 + nt] += 1
+    for s in range(n_seq):
+        if int(q_len[s]) == 1:
+            continue
+        for kh in range(num_kv_heads):
+            c = cover.get((s, kh))
+            if c is None or np.any(c != 1):
+                fail(f"seq {s} head {kh}: new tokens not covered exactly once")
+    work = np.asarray(work, dtype=np.int64).reshape(-1, WORK_INTS)
+    waiting = 0
+    for it in work[:num_prefill]:
+        pos0 = int(it[W_QPOS0]) - int(it[W_QTOK0])
+        if (int(it[W_KVEND]) - 1) // PAGE >= pos0 // PAGE:
+            waiting += 1
+    if waiting != num_waiting:
+        fail(f"{num_waiting} waiting units reported, {waiting} read a page with a new token")
+    return {"records": len(records), "waiting": waiting}

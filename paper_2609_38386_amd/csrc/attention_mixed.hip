@@ -34,6 +34,13 @@
 // and bumps its group's counter; the last arriver acquires and merges all
 // splits in split-index order (deterministic), writes the output and resets
 // the counter to zero for the next launch.
+//
+// The same kernel, instantiated with APP, also writes the iteration's new
+// keys and values into the cache (the append and the attention in one
+// launch): a decode unit takes its own new token from k_new / v_new into its
+// staged last page and stores it to its slot; leading append workgroups write
+// the prompt tokens, and prefill units wait for them before loading a page
+// that holds a new token.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -88,6 +95,14 @@ struct Args {
   int32_t decode_waves;  // wavefronts of the decode workgroups of this launch
   int32_t decode_static; // decode units handed out by position, the rest by queue
   float scale_log2;      // softmax scale * log2(e)
+  // Append launches only: this iteration's keys and values [tokens][hkv][128],
+  // the leading workgroups that write the append records stored after the
+  // units, and the prefill units that wait for them.
+  const uint16_t* k_new;
+  const uint16_t* v_new;
+  int32_t app_wgs;
+  int32_t num_append;
+  int32_t num_waiting;
 };
 
 __device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
@@ -169,9 +184,40 @@ __device__ __forceinline__ int* group_counter_ptr(float* ws, int grp) {
 __device__ __forceinline__ int* header_word(float* ws, int i) { return reinterpret_cast<int*>(ws) + i; }
 constexpr int HDR_TICKET = DLFP_WORKSPACE_TICKET_WORD;
 constexpr int HDR_DONE = DLFP_WORKSPACE_DONE_WORD;
+// Append launches: append wavefronts finished, waiting prefill units finished.
+constexpr int HDR_APPEND = DLFP_WORKSPACE_APPEND_WORD;
+constexpr int HDR_WAITED = DLFP_WORKSPACE_WAITED_WORD;
 
-__device__ __forceinline__ void raise_error(float* ws) {
-  __hip_atomic_store(reinterpret_cast<int*>(ws), 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+// Error word values: 1 = a block id outside the pool, 2 = a wait for the
+// append records ran out.
+__device__ __forceinline__ void raise_error(float* ws, int code = 1) {
+  __hip_atomic_store(reinterpret_cast<int*>(ws), code, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Append launches.  A prefill unit polls the count of finished append
+// workgroups (device-coherent loads, so a stale L2 line is never returned)
+// until all have counted themselves; the append workgroups come first in the
+// grid and wait for nothing, so they are dispatched before any waiting unit
+// and the count is reached.  The poll is bounded all the same: after about
+// a second it raises error 2 and goes on.  A waiting unit counts itself on
+// a second word once its loop is done (it never polls again); the last one
+// zeroes both words for the next launch.  No page that holds a new token is
+// read before the wait, so no XCD's L2 holds an old copy of one.
+constexpr int APPEND_SPIN_LIMIT = 1 << 20;
+
+__device__ __forceinline__ void wait_for_appends(const Args& a) {
+  const int* done = header_word(a.ws, HDR_APPEND);
+  const int need = a.app_wgs;
+  for (int spins = 0;; ++spins) {
+    const int n = uniform(__hip_atomic_load(done, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+    if (n >= need) break;
+    if (spins == APPEND_SPIN_LIMIT) {
+      if ((threadIdx.x & 63) == 0) raise_error(a.ws, 2);
+      break;
+    }
+    __builtin_amdgcn_s_sleep(8);
+  }
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
 // Split-K partial results cross workgroups (and XCDs, whose L2s are not
@@ -388,7 +434,7 @@ __device__ __forceinline__ void prefill_merge(const Args& a, const Slots sl, int
   }
 }
 
-template <int G>
+template <int G, bool APP>
 __device__ void prefill_unit(const Args& a, const int32_t* it, char* smem, int* flag) {
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int col = lane & 31, hi = lane >> 5;
@@ -420,6 +466,14 @@ __device__ void prefill_unit(const Args& a, const int32_t* it, char* smem, int* 
 
   const int ntiles = (ke - kb + KV_TILE - 1) / KV_TILE;
   const int first_page = kb / PAGE, last_page = (ke - 1) / PAGE;
+  // Append launches: the first tile with a page at or past the one holding
+  // the sequence's first new token (the unit waits before loading it).
+  int wait_tile = ntiles;
+  if constexpr (APP) {
+    const int newp = pos0 / PAGE;
+    if (a.app_wgs > 0 && last_page >= newp)
+      wait_tile = max(0, (newp - first_page) >> 2);  // wave 3's page
+  }
   int32_t* ptab = reinterpret_cast<int32_t*>(smem + PTAB_BASE);
   for (int i = tid; i <= last_page - first_page; i += THREADS) ptab[i] = bt[first_page + i];
   wait_memory_complete();  // queries and block ids resident before the KV pipeline starts
@@ -574,6 +628,13 @@ __device__ void prefill_unit(const Args& a, const int32_t* it, char* smem, int* 
   // Prologue: tiles 0 (K and V) and 1 (K) in flight, then S_0.  off_next
   // carries the page of tile j + 1 from the step that loaded its keys to the
   // step that loads its values.
+  // The wait for the append records sits outside the tile loop (which is
+  // split there): inside it, the poll's control flow costs the loop body its
+  // partial LDS waits.  Tile t's keys are issued in the prologue (t < 2) or
+  // by step t - 2.
+  if constexpr (APP) {
+    if (wait_tile <= 1) wait_for_appends(a);
+  }
   int64_t off_next = page_off(0);
   issue_k(off_next, 0);
   issue_v(off_next, 0);
@@ -648,10 +709,44 @@ __device__ void prefill_unit(const Args& a, const int32_t* it, char* smem, int* 
       __syncthreads();
     }
   };
-  for (int j = 0; j < ntiles; j += 2) {
-    step(j, sa, sb, std::integral_constant<int, 0>{});
-    if (j + 1 < ntiles) step(j + 1, sb, sa, std::integral_constant<int, 1>{});
+  const std::integral_constant<int, 0> even;
+  const std::integral_constant<int, 1> odd;
+  int j = 0;
+  if constexpr (APP) {
+    if (wait_tile > 1 && wait_tile < ntiles) {
+      const int jw = wait_tile - 2;  // the step that issues tile wait_tile
+      for (; j + 1 < jw; j += 2) {
+        step(j, sa, sb, even);
+        step(j + 1, sb, sa, odd);
+      }
+      if (j < jw) step(j++, sa, sb, even);
+      wait_for_appends(a);
+      if (j & 1) step(j++, sb, sa, odd);
+    }
   }
+  for (; j < ntiles; j += 2) {
+    step(j, sa, sb, even);
+    if (j + 1 < ntiles) step(j + 1, sb, sa, odd);
+  }
+
+  // A waiting unit counts itself past its wait; the count returns while the
+  // results are stored, and the last such unit zeroes the append words.
+  int waited = -1;
+  if constexpr (APP) {
+    if (wait_tile < ntiles && tid == 0)
+      waited = __hip_atomic_fetch_add(header_word(a.ws, HDR_WAITED), 1, __ATOMIC_RELAXED,
+                                      __HIP_MEMORY_SCOPE_AGENT);
+  }
+  auto reset_append_words = [&]() {
+    if constexpr (APP) {
+      if (waited >= 0 && waited == a.num_waiting - 1) {
+        __hip_atomic_store(header_word(a.ws, HDR_APPEND), 0, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(header_word(a.ws, HDR_WAITED), 0, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+  };
 
   l_run = sum_xor32(l_run);
   const int rows = nt * G;
@@ -667,6 +762,7 @@ __device__ void prefill_unit(const Args& a, const int32_t* it, char* smem, int* 
           store4(a, orow + mb * 32 + 8 * g4 + 4 * hi, o[mb][4 * g4] * inv,
                  o[mb][4 * g4 + 1] * inv, o[mb][4 * g4 + 2] * inv, o[mb][4 * g4 + 3] * inv);
     }
+    reset_append_words();
     return;
   }
 
@@ -692,6 +788,7 @@ __device__ void prefill_unit(const Args& a, const int32_t* it, char* smem, int* 
     }
   }
   wait_memory_complete();
+  reset_append_words();
   __syncthreads();  // every wave of the unit has completed its stores
   const int grp = it[DLFP_W_GROUP];
   if (tid == 0) *flag = arrive(a.ws, grp) == nsplits - 1;
@@ -715,7 +812,7 @@ __device__ void prefill_unit(const Args& a, const int32_t* it, char* smem, int* 
 // Wave-private LDS slice: K page (token rows, 16-byte chunk x of row R at
 // x ^ 8 (R & 1)), V^T page (64-byte dim-pair region r, 16-byte slot i at
 // (i + r / 4) & 3), then the probability buffer p[head][16 keys] in bf16.
-template <int G>
+template <int G, bool APP>
 __device__ void decode_unit(const Args& a, const int32_t* it, char* wl) {
   const int lane = threadIdx.x & 63;
   const int kg = lane >> 3, c = lane & 7;
@@ -753,8 +850,33 @@ __device__ void decode_unit(const Args& a, const int32_t* it, char* wl) {
   }
   const int p_begin = kb / PAGE, p_end = (ke + PAGE - 1) / PAGE;
   for (int i = lane; i < p_end - p_begin; i += 64) ptab[i] = bt[p_begin + i];
+  // Append launches: the unit whose keys end with the sequence's new token
+  // (position QPOS0) loads that token's key row (lanes 0-15, 16 bytes each)
+  // and its values of dims 2 lane, 2 lane + 1, writes them to their slot, and
+  // puts them into the staged page in place of what the cache held there.
+  const int newpos = uniform(it[DLFP_W_QPOS0]);
+  const bool own_new = APP && newpos < ke;
+  const int new_page = newpos / PAGE, new_off = newpos % PAGE;
+  u32x4_t kn = {0u, 0u, 0u, 0u};
+  uint32_t vn = 0u;
+  if (own_new) {
+    const int64_t src = ((int64_t)tok * a.hkv + kh) * D;
+    if (lane < 16) kn = *reinterpret_cast<const u32x4_t*>(a.k_new + src + 8 * lane);
+    vn = *reinterpret_cast<const uint32_t*>(a.v_new + src + 2 * lane);
+  }
   wait_memory_complete();  // queries and block ids resident before the page pipeline starts
   wave_sync();
+  if (own_new) {
+    const int raw = ptab[new_page - p_begin];
+    if ((unsigned)raw < (unsigned)a.num_blocks) {
+      const int64_t base = ((int64_t)raw * a.hkv + kh) * PAGE_ELEMS;
+      uint16_t* kc = const_cast<uint16_t*>(a.kc);
+      uint16_t* vc = const_cast<uint16_t*>(a.vc);
+      if (lane < 16) *reinterpret_cast<u32x4_t*>(kc + base + new_off * D + 8 * lane) = kn;
+      vc[base + (2 * lane) * PAGE + vt_pos(new_off)] = (uint16_t)(vn & 0xFFFFu);
+      vc[base + (2 * lane + 1) * PAGE + vt_pos(new_off)] = (uint16_t)(vn >> 16);
+    }
+  }
   float m[G], l[G], o0[G], o1[G];
 #pragma unroll
   for (int h = 0; h < G; ++h) {
@@ -803,6 +925,17 @@ __device__ void decode_unit(const Args& a, const int32_t* it, char* wl) {
       *reinterpret_cast<u32x4_t*>(vl + rg * 64 + (((si + (rg >> 2)) & 3) << 4)) = v;
     }
     fetch(k4, v4, p + NSLOT);
+    if (own_new && p == new_page) {
+      wave_sync();  // the staged copies land first
+      if (lane < 16)
+        *reinterpret_cast<u32x4_t*>(kl + new_off * 256 + ((lane ^ ((new_off & 1) << 3)) << 4)) = kn;
+      // region lane holds dim 2 lane in slots 0-1 and dim 2 lane + 1 in slots 2-3
+      const int sp = vt_pos(new_off), half = sp >> 3;
+      char* v0 = vl + lane * 64 + (((half + (lane >> 2)) & 3) << 4) + 2 * (sp & 7);
+      char* v1 = vl + lane * 64 + (((2 + half + (lane >> 2)) & 3) << 4) + 2 * (sp & 7);
+      *reinterpret_cast<uint16_t*>(v0) = (uint16_t)(vn & 0xFFFFu);
+      *reinterpret_cast<uint16_t*>(v1) = (uint16_t)(vn >> 16);
+    }
     wave_sync();  // staged page visible to every lane
 
     // Keys 8 st + kg of the page (st = 0, 1): each lane holds 16 dims of both.
@@ -1008,16 +1141,120 @@ __device__ void decode_unit(const Args& a, const int32_t* it, char* wl) {
     __hip_atomic_store(group_counter(a.ws, grp), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// ---------------------------------------------------------------- append
+
+// Append workgroup (append launches): each wavefront writes whole append
+// records, one at a time -- one run of a prompt sequence's new tokens inside
+// one page, for one KV head.  Key rows: lane covers 16-byte chunk lane % 16
+// of rows 4 j + lane / 16.  Values: lane owns dims 2 lane and 2 lane + 1 and
+// gathers them with one 4-byte load per token (a wavefront reads the whole
+// 256-byte value row); a record that fills its page is written as whole
+// 32-byte V^T rows, any other as one 2-byte value per token and dim (the
+// page's other slots are left alone).  Every load of a record is issued
+// before its stores.  The stores are ordinary ones, which the XCD's L2
+// combines into whole lines (written through one by one, the half-line
+// pieces cost a read-modify-write each at the memory side; measured 60-70 us
+// for a 2048-token chunk).  When prefill units of the launch wait for the
+// records, the workgroup then writes its L2 back (an agent-scope release) and
+// counts itself done.
+
+__device__ void append_records(const Args& a) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  uint16_t* kc = const_cast<uint16_t*>(a.kc);
+  uint16_t* vc = const_cast<uint16_t*>(a.vc);
+  const int x16 = lane & 15;
+  for (int r = blockIdx.x * 4 + wave; r < a.num_append; r += 4 * a.app_wgs) {
+    const int32_t* it = a.work + (int64_t)(a.num_units + r) * DLFP_WORK_INTS;
+    const int s = uniform(it[DLFP_W_SEQ]), kh = uniform(it[DLFP_W_KVHEAD]);
+    const int n = uniform(it[DLFP_W_QNTOK]), row0 = uniform(it[DLFP_W_QROW0]);
+    const int pos = uniform(it[DLFP_W_QPOS0]);
+    const int o0 = pos % PAGE, o1 = o0 + n;
+    const int raw = uniform(a.block_table[(int64_t)s * a.max_blocks + pos / PAGE]);
+    if ((unsigned)raw >= (unsigned)a.num_blocks || o1 > PAGE) {
+      if (lane == 0) raise_error(a.ws);
+      continue;
+    }
+    const int64_t base = ((int64_t)raw * a.hkv + kh) * PAGE_ELEMS;
+    // token row of slot o in k_new / v_new: row0 + o - o0
+    const int64_t src0 = ((int64_t)(row0 - o0) * a.hkv + kh) * D;
+    const int64_t tok_stride = (int64_t)a.hkv * D;
+    u32x4_t kr[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int o = 4 * j + (lane >> 4);
+      kr[j] = o >= o0 && o < o1
+                  ? *reinterpret_cast<const u32x4_t*>(a.k_new + src0 + o * tok_stride + 8 * x16)
+                  : u32x4_t{0u, 0u, 0u, 0u};
+    }
+    uint32_t x[PAGE];
+#pragma unroll
+    for (int o = 0; o < PAGE; ++o)
+      x[o] = o >= o0 && o < o1
+                 ? *reinterpret_cast<const uint32_t*>(a.v_new + src0 + o * tok_stride + 2 * lane)
+                 : 0u;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int o = 4 * j + (lane >> 4);
+      if (o >= o0 && o < o1) *reinterpret_cast<u32x4_t*>(kc + base + o * D + 8 * x16) = kr[j];
+    }
+    uint16_t* row = vc + base + (2 * lane) * PAGE;  // rows 2 lane and 2 lane + 1
+    if (o0 == 0 && o1 == PAGE) {
+      // position 2 w + i of a row holds slot vt_pos(2 w + i)
+      u32x4_t lo[2], hi[2];
+#pragma unroll
+      for (int w = 0; w < 8; ++w) {
+        const uint32_t xa = x[vt_pos(2 * w)], xb = x[vt_pos(2 * w + 1)];
+        lo[w >> 2][w & 3] = (xa & 0xFFFFu) | (xb << 16);
+        hi[w >> 2][w & 3] = (xa >> 16) | (xb & 0xFFFF0000u);
+      }
+      u32x4_t* dst = reinterpret_cast<u32x4_t*>(row);
+      dst[0] = lo[0];
+      dst[1] = lo[1];
+      dst[2] = hi[0];
+      dst[3] = hi[1];
+    } else {
+#pragma unroll
+      for (int o = 0; o < PAGE; ++o)
+        if (o >= o0 && o < o1) {
+          row[vt_pos(o)] = (uint16_t)(x[o] & 0xFFFFu);
+          row[PAGE + vt_pos(o)] = (uint16_t)(x[o] >> 16);
+        }
+    }
+  }
+  if (a.num_waiting > 0) {
+    wait_memory_complete();  // this wavefront's stores have reached the L2
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");  // write the L2 back
+      __hip_atomic_fetch_add(header_word(a.ws, HDR_APPEND), 1, __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+}
+
+// The append records alone, as a launch of their own (one record per
+// wavefront) ahead of the attention launch.
+__global__ __launch_bounds__(THREADS) void append_records_kernel(Args a) { append_records(a); }
+
 // ---------------------------------------------------------------- kernel
 
-template <int G>
+template <int G, bool APP>
 __global__ __launch_bounds__(THREADS, 2) void attention_mixed_kernel(Args a) {
   __shared__ __attribute__((aligned(16))) char smem[LDS_BYTES];
   __shared__ int flag;
-  const int b = blockIdx.x;
+  int b = blockIdx.x;
+  if constexpr (APP) {
+    // Append workgroups first (a multiple of 8, so the XCD of every later
+    // workgroup is unchanged by the offset).
+    if (b < a.app_wgs) {
+      append_records(a);
+      return;
+    }
+    b -= a.app_wgs;
+  }
   if (b < a.num_prefill) {
     const int u = xcd_remap(b, a.num_prefill);
-    prefill_unit<G>(a, a.work + (int64_t)u * DLFP_WORK_INTS, smem, &flag);
+    prefill_unit<G, APP>(a, a.work + (int64_t)u * DLFP_WORK_INTS, smem, &flag);
   } else {
     // Decode wavefront w of decode workgroup d starts with unit 4 d + w when
     // that is one of the first decode_static units (the workgroups resident
@@ -1041,7 +1278,7 @@ __global__ __launch_bounds__(THREADS, 2) void attention_mixed_kernel(Args a) {
     int t = (b - a.num_prefill) * 4 + wave;
     if (queue && t >= a.decode_static) t = ticket();
     while (t < ndec) {
-      decode_unit<G>(a, a.work + (int64_t)(a.num_prefill + t) * DLFP_WORK_INTS, wl);
+      decode_unit<G, APP>(a, a.work + (int64_t)(a.num_prefill + t) * DLFP_WORK_INTS, wl);
       wave_sync();
       if (!queue) break;
       t = ticket();
@@ -1081,21 +1318,21 @@ int compute_units() {
   return cached[dev];
 }
 
-template <int G>
+constexpr int FUSED_APPEND_MAX_WGS = 16;
+
+template <int G, bool APP>
 hipError_t launch(const Args& a, int grid, hipStream_t stream) {
-  attention_mixed_kernel<G><<<grid, THREADS, 0, stream>>>(a);
+  attention_mixed_kernel<G, APP><<<grid, THREADS, 0, stream>>>(a);
   return hipGetLastError();
 }
 
-}  // namespace
-
-extern "C" int dlfp_attention_mixed(const dlfp_dims* dims, const dlfp_meta* meta,
-                                    const int32_t* d_work,
-                                    const int32_t* d_block_table, int32_t max_blocks,
-                                    int32_t num_blocks, const void* q, const void* k_cache,
-                                    const void* v_cache, float scale, void* out,
-                                    int32_t out_dtype, void* workspace, size_t workspace_bytes,
-                                    hipStream_t stream) {
+// Validation, grid and launch shared by both entry points; k_new / v_new are
+// null for the attention-only launch.
+int launch_mixed(const dlfp_dims* dims, const dlfp_meta* meta, const int32_t* d_work,
+                 const int32_t* d_block_table, int32_t max_blocks, int32_t num_blocks,
+                 const void* q, const void* k_new, const void* v_new, const void* k_cache,
+                 const void* v_cache, float scale, void* out, int32_t out_dtype, void* workspace,
+                 size_t workspace_bytes, hipStream_t stream) {
   int g = 0;
   const int st = dlfp::check_dims(dims, &g);
   if (st != DLFP_OK) return st;
@@ -1105,9 +1342,15 @@ extern "C" int dlfp_attention_mixed(const dlfp_dims* dims, const dlfp_meta* meta
   if (meta->num_units < 0 || meta->num_prefill_units < 0 ||
       meta->num_prefill_units > meta->num_units || meta->num_groups < 0)
     return DLFP_EINVAL;
+  const bool app = k_new != nullptr;
+  if (app && (meta->num_append < 0 || meta->num_waiting_units < 0 ||
+              (meta->num_append > 0 && meta->num_waiting_units == 0) ||
+              meta->num_waiting_units > meta->num_prefill_units))
+    return DLFP_EINVAL;
   if (meta->num_units == 0) return DLFP_OK;
   if (!d_work || !d_block_table || !q || !k_cache || !v_cache || !out || !workspace)
     return DLFP_EINVAL;
+  if (app && !v_new) return DLFP_EINVAL;
   if (max_blocks <= 0 || num_blocks <= 0) return DLFP_EINVAL;
   if ((int64_t)workspace_bytes < meta->workspace_bytes ||
       workspace_bytes < (size_t)DLFP_WORKSPACE_PARTIALS)
@@ -1129,27 +1372,77 @@ extern "C" int dlfp_attention_mixed(const dlfp_dims* dims, const dlfp_meta* meta
   a.num_prefill = meta->num_prefill_units;
   a.out_f32 = out_dtype;
   a.scale_log2 = scale * LOG2E;
+  a.k_new = static_cast<const uint16_t*>(k_new);
+  a.v_new = static_cast<const uint16_t*>(v_new);
+  a.num_append = app ? meta->num_append : 0;
+  a.num_waiting = app ? meta->num_waiting_units : 0;
+  // Append workgroups in the launch: about two records per wavefront, a
+  // multiple of 8.  Past FUSED_APPEND_MAX_WGS of them the records get a launch
+  // of their own first: at the start of the attention launch each append
+  // workgroup holds a CU slot, which pushes long prefill units to share CUs
+  // (measured on Qwen3-0.6B shapes: chunks of 512-2048 prompt tokens took
+  // 15-20% longer in one launch, while chunks of 64-256 gained 6-8% per
+  // iteration from dropping the second launch).
+  a.app_wgs = a.num_append > 0 ? (int)(((int64_t)a.num_append + 63) / 64 * 8) : 0;
+  if (a.app_wgs > FUSED_APPEND_MAX_WGS) {
+    Args r = a;
+    r.app_wgs = (a.num_append + 3) / 4;
+    r.num_waiting = 0;
+    (void)hipGetLastError();
+    append_records_kernel<<<r.app_wgs, THREADS, 0, stream>>>(r);
+    if (hipGetLastError() != hipSuccess) return DLFP_EHIP;
+    a.app_wgs = 0;
+    a.num_append = 0;
+    a.num_waiting = 0;
+  }
   // Decode workgroups: enough to fill the resident slots of the device (two
   // per CU), fewer when there are fewer units; they drain the decode queue.
-  // Only those that find a slot left by the prefill workgroups from the start
-  // (at least 64) get units by position.
+  // Only those that find a slot left by the append and prefill workgroups
+  // from the start (at least 64) get units by position.
   const int cus = compute_units();
   const int decode_units = meta->num_units - meta->num_prefill_units;
   const int decode_wgs = std::min((decode_units + 3) / 4, 2 * cus);
-  const int slots = meta->num_prefill_units < 2 * cus
-                        ? std::max(2 * cus - meta->num_prefill_units, 64) : 2 * cus;
+  const int ahead = meta->num_prefill_units + a.app_wgs;
+  const int slots = ahead < 2 * cus ? std::max(2 * cus - ahead, 64) : 2 * cus;
   a.decode_waves = 4 * decode_wgs;
   a.decode_static = std::min(decode_units, 4 * std::min(decode_wgs, slots));
-  const int grid = meta->num_prefill_units + decode_wgs;
+  const int grid = a.app_wgs + meta->num_prefill_units + decode_wgs;
   (void)hipGetLastError();
   hipError_t e;
   switch (g) {
-    case 1: e = launch<1>(a, grid, stream); break;
-    case 2: e = launch<2>(a, grid, stream); break;
-    case 4: e = launch<4>(a, grid, stream); break;
-    default: e = launch<8>(a, grid, stream); break;
+    case 1: e = app ? launch<1, true>(a, grid, stream) : launch<1, false>(a, grid, stream); break;
+    case 2: e = app ? launch<2, true>(a, grid, stream) : launch<2, false>(a, grid, stream); break;
+    case 4: e = app ? launch<4, true>(a, grid, stream) : launch<4, false>(a, grid, stream); break;
+    default: e = app ? launch<8, true>(a, grid, stream) : launch<8, false>(a, grid, stream); break;
   }
   return e == hipSuccess ? DLFP_OK : DLFP_EHIP;
+}
+
+}  // namespace
+
+extern "C" int dlfp_attention_mixed(const dlfp_dims* dims, const dlfp_meta* meta,
+                                    const int32_t* d_work,
+                                    const int32_t* d_block_table, int32_t max_blocks,
+                                    int32_t num_blocks, const void* q, const void* k_cache,
+                                    const void* v_cache, float scale, void* out,
+                                    int32_t out_dtype, void* workspace, size_t workspace_bytes,
+                                    hipStream_t stream) {
+  return launch_mixed(dims, meta, d_work, d_block_table, max_blocks, num_blocks, q, nullptr,
+                      nullptr, k_cache, v_cache, scale, out, out_dtype, workspace,
+                      workspace_bytes, stream);
+}
+
+extern "C" int dlfp_append_attention_mixed(const dlfp_dims* dims, const dlfp_meta* meta,
+                                           const int32_t* d_work, const int32_t* d_block_table,
+                                           int32_t max_blocks, int32_t num_blocks, const void* q,
+                                           const void* k_new, const void* v_new, void* k_cache,
+                                           void* v_cache, float scale, void* out,
+                                           int32_t out_dtype, void* workspace,
+                                           size_t workspace_bytes, hipStream_t stream) {
+  if (!k_new || !v_new) return DLFP_EINVAL;
+  return launch_mixed(dims, meta, d_work, d_block_table, max_blocks, num_blocks, q, k_new,
+                      v_new, k_cache, v_cache, scale, out, out_dtype, workspace,
+                      workspace_bytes, stream);
 }
 
 extern "C" int dlfp_workspace_init(void* workspace, size_t workspace_bytes, hipStream_t stream) {

@@ -356,6 +356,43 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
     u.f[DLFP_W_WSOFF] = (int32_t)(group_off[grp] + u.f[DLFP_W_SPLIT] * slot);
   }
 
+  // Append records for the one-launch cache write: each prompt sequence's new
+  // tokens cut at page boundaries, per KV head (decode units write their own
+  // token).  A prefill unit waits for them when its last key lies in a page
+  // from the one holding its sequence's first new token on.
+  std::vector<Unit> appends;
+  for (int s = 0; s < num_seqs; ++s) {
+    if (q_len[s] == 1) continue;
+    const int64_t pos0 = kv_len[s] - q_len[s];
+    for (int kh = 0; kh < hkv; ++kh)
+      for (int64_t p = pos0; p < kv_len[s];) {
+        const int64_t n = std::min<int64_t>(DLFP_PAGE_SIZE - p % DLFP_PAGE_SIZE, kv_len[s] - p);
+        Unit u;
+        std::memset(&u, 0, sizeof(u));
+        u.f[DLFP_W_SEQ] = s;
+        u.f[DLFP_W_KVHEAD] = kh;
+        u.f[DLFP_W_QTOK0] = (int32_t)(p - pos0);
+        u.f[DLFP_W_QNTOK] = (int32_t)n;
+        u.f[DLFP_W_KVBEGIN] = (int32_t)p;
+        u.f[DLFP_W_KVEND] = (int32_t)(p + n);
+        u.f[DLFP_W_GROUP] = -1;
+        u.f[DLFP_W_NSPLITS] = 1;
+        u.f[DLFP_W_KIND] = DLFP_KIND_APPEND;
+        u.f[DLFP_W_QROW0] = (int32_t)(cu_q_of[s] + p - pos0);
+        u.f[DLFP_W_QPOS0] = (int32_t)p;
+        appends.push_back(u);
+        p += n;
+      }
+  }
+  int64_t waiting = 0;
+  for (int64_t i = 0; i < num_prefill; ++i) {
+    const Unit& u = units[i];
+    const int64_t pos0 = u.f[DLFP_W_QPOS0] - u.f[DLFP_W_QTOK0];
+    if ((u.f[DLFP_W_KVEND] - 1) / DLFP_PAGE_SIZE >= pos0 / DLFP_PAGE_SIZE) ++waiting;
+  }
+  const int64_t records = (int64_t)(units.size() + appends.size());
+  if (records > std::numeric_limits<int32_t>::max() / DLFP_WORK_INTS) return DLFP_ERANGE;
+
   meta->num_seqs = num_seqs;
   meta->num_tokens = (int32_t)tokens;
   meta->num_units = (int32_t)units.size();
@@ -364,11 +401,12 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
   meta->decode_split_tokens = (int32_t)split_d;
   meta->prefill_split_tokens = (int32_t)split_p;
   meta->workspace_bytes = std::max<int64_t>(off * 4, partial_base_bytes);
-  if (meta->cap_seqs < num_seqs || meta->cap_tokens < tokens ||
-      meta->cap_work < (int64_t)units.size())
+  meta->num_append = (int32_t)appends.size();
+  meta->num_waiting_units = (int32_t)waiting;
+  if (meta->cap_seqs < num_seqs || meta->cap_tokens < tokens || meta->cap_work < records)
     return DLFP_ENOSPC;
   if ((num_seqs > 0 && (!meta->cu_q || !meta->q_pos0)) || (tokens > 0 && !meta->slot_mapping) ||
-      (!units.empty() && !meta->work))
+      (records > 0 && !meta->work))
     return DLFP_EINVAL;
   if (meta->cu_q) meta->cu_q[0] = 0;
   int64_t t = 0;
@@ -384,6 +422,9 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
   }
   for (size_t u = 0; u < units.size(); ++u)
     std::memcpy(meta->work + u * DLFP_WORK_INTS, units[u].f, sizeof(units[u].f));
+  for (size_t r = 0; r < appends.size(); ++r)
+    std::memcpy(meta->work + (units.size() + r) * DLFP_WORK_INTS, appends[r].f,
+                sizeof(appends[r].f));
   return DLFP_OK;
 }
 

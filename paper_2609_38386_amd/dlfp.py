@@ -56,7 +56,8 @@ class dlfp_meta(ctypes.Structure):
                 ("num_seqs", ctypes.c_int32), ("num_tokens", ctypes.c_int32),
                 ("num_units", ctypes.c_int32), ("num_prefill_units", ctypes.c_int32),
                 ("num_groups", ctypes.c_int32), ("decode_split_tokens", ctypes.c_int32),
-                ("prefill_split_tokens", ctypes.c_int32), ("workspace_bytes", ctypes.c_int64)]
+                ("prefill_split_tokens", ctypes.c_int32), ("workspace_bytes", ctypes.c_int64),
+                ("num_append", ctypes.c_int32), ("num_waiting_units", ctypes.c_int32)]
 
 
 class dlfp_controller(ctypes.Structure):
@@ -66,6 +67,7 @@ class dlfp_controller(ctypes.Structure):
 
 
 EXPORTS = ["dlfp_build_varlen_meta", "dlfp_kv_append", "dlfp_attention_mixed",
+           "dlfp_append_attention_mixed",
            "dlfp_workspace_init", "dlfp_workspace_error", "dlfp_controller_init",
            "dlfp_controller_step", "dlfp_timer_create", "dlfp_timer_destroy", "dlfp_timer_start",
            "dlfp_timer_stop", "dlfp_timer_elapsed_ms", "dlfp_stream_hold", "dlfp_status_string",
@@ -93,6 +95,10 @@ def lib():
     L.dlfp_attention_mixed.argtypes = [ctypes.POINTER(dlfp_dims), ctypes.POINTER(dlfp_meta),
                                        vp, vp, i32, i32, vp, vp, vp, ctypes.c_float,
                                        vp, i32, vp, sz, vp]
+    L.dlfp_append_attention_mixed.argtypes = [ctypes.POINTER(dlfp_dims),
+                                              ctypes.POINTER(dlfp_meta), vp, vp, i32, i32, vp,
+                                              vp, vp, vp, vp, ctypes.c_float, vp, i32, vp, sz,
+                                              vp]
     L.dlfp_workspace_init.argtypes = [vp, sz, vp]
     L.dlfp_workspace_error.argtypes = [vp, _P32, vp]
     L.dlfp_controller_init.argtypes = [ctypes.POINTER(dlfp_controller), ctypes.c_double, i32, i32,
@@ -162,6 +168,15 @@ class Meta:
     def work(self) -> np.ndarray:
         return self.work_buf[:self.c.num_units]
 
+    @property
+    def append_records(self) -> np.ndarray:
+        return self.work_buf[self.c.num_units:self.c.num_units + self.c.num_append]
+
+    @property
+    def records(self) -> np.ndarray:
+        """Units followed by append records: what the device copy of the work list holds."""
+        return self.work_buf[:self.c.num_units + self.c.num_append]
+
 
 def dlfp_build_varlen_meta(dims: dlfp_dims, q_len, kv_len, block_table: np.ndarray,
                            num_blocks: int, tuning: Optional[dlfp_tuning] = None) -> Meta:
@@ -180,7 +195,7 @@ def dlfp_build_varlen_meta(dims: dlfp_dims, q_len, kv_len, block_table: np.ndarr
                                   ctypes.byref(probe.c))
     if st not in (0, -3):
         _check(st, "dlfp_build_varlen_meta")
-    meta = Meta(probe.c.num_seqs, probe.c.num_tokens, probe.c.num_units)
+    meta = Meta(probe.c.num_seqs, probe.c.num_tokens, probe.c.num_units + probe.c.num_append)
     st = L.dlfp_build_varlen_meta(ctypes.byref(dims), ctypes.byref(tn), n, _ptr32(q_len),
                                   _ptr32(kv_len), _ptr32(bt), bt.shape[1], int(num_blocks),
                                   ctypes.byref(meta.c))
@@ -211,6 +226,20 @@ def dlfp_attention_mixed(dims: dlfp_dims, meta: Meta, d_work, d_block_table, q, 
         _dptr(out), out_dtype, _dptr(workspace), int(workspace.numel() * workspace.element_size()),
         _stream(stream))
     _check(st, "dlfp_attention_mixed")
+
+
+def dlfp_append_attention_mixed(dims: dlfp_dims, meta: Meta, d_work, d_block_table, q, k_new,
+                                v_new, k_cache, v_cache, scale: float, out, workspace,
+                                stream=None) -> None:
+    """dlfp_kv_append + dlfp_attention_mixed in one launch; d_work holds meta.records."""
+    import torch
+    out_dtype = {torch.bfloat16: 0, torch.float32: 1}[out.dtype]
+    st = lib().dlfp_append_attention_mixed(
+        ctypes.byref(dims), ctypes.byref(meta.c), _dptr(d_work), _dptr(d_block_table),
+        int(d_block_table.shape[1]), int(k_cache.shape[0]), _dptr(q), _dptr(k_new),
+        _dptr(v_new), _dptr(k_cache), _dptr(v_cache), float(scale), _dptr(out), out_dtype,
+        _dptr(workspace), int(workspace.numel() * workspace.element_size()), _stream(stream))
+    _check(st, "dlfp_append_attention_mixed")
 
 
 def dlfp_workspace_init(workspace, stream=None) -> None:

@@ -319,9 +319,9 @@ class GpuExecutor:
         # the layer's device work and not the host's launch gaps.
         D.dlfp_stream_hold(self.hold_us)
         self.timer.start()
-        D.dlfp_kv_append(self.dims, self.k[:T], self.v[:T], st.d_slots, self.pool.k, self.pool.v)
-        D.dlfp_attention_mixed(self.dims, st.meta, st.d_work, d_bt, self.q[:T], self.pool.k,
-                               self.pool.v, self.scale, self.out[:T], ws)
+        D.dlfp_append_attention_mixed(self.dims, st.meta, st.d_work, d_bt, self.q[:T],
+                                      self.k[:T], self.v[:T], self.pool.k, self.pool.v,
+                                      self.scale, self.out[:T], ws)
         self.timer.stop()
         return self.timer.elapsed_ms()
 

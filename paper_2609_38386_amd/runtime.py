@@ -77,7 +77,8 @@ class Batch:
                                               num_blocks, tuning)
         m = self.meta
         self.num_tokens = m.num_tokens
-        host = np.concatenate([m.slot_mapping[:m.num_tokens], m.work.reshape(-1)]).astype(np.int32)
+        host = np.concatenate([m.slot_mapping[:m.num_tokens], m.records.reshape(-1)]
+                              ).astype(np.int32)
         dev = torch.from_numpy(host).to(device)
         self.d_slots = dev[:m.num_tokens]
         self.d_work = dev[m.num_tokens:]
@@ -94,6 +95,13 @@ class Batch:
         ws = workspace.ensure(self.meta.workspace_bytes, self.meta.num_groups, stream)
         _d.dlfp_attention_mixed(self.dims, self.meta, self.d_work, self.d_block_table, q,
                                 pool.k, pool.v, scale, out, ws, stream)
+
+    def append_attention(self, pool: KVPool, q: torch.Tensor, k_new: torch.Tensor,
+                         v_new: torch.Tensor, scale: float, out: torch.Tensor,
+                         workspace: Workspace, stream=None):
+        ws = workspace.ensure(self.meta.workspace_bytes, self.meta.num_groups, stream)
+        _d.dlfp_append_attention_mixed(self.dims, self.meta, self.d_work, self.d_block_table, q,
+                                       k_new, v_new, pool.k, pool.v, scale, out, ws, stream)
 
 
 class Iteration:
@@ -136,12 +144,21 @@ class Iteration:
                         bits_to_device(s.stream.v[:s.pos0], self.device))
 
     def run(self, workspace: Workspace, scale: float, out_dtype=torch.bfloat16,
-            append: bool = True, out: Optional[torch.Tensor] = None) -> torch.Tensor:
-        if append:
-            self.batch.append(self.pool, self.k_new, self.v_new)
+            append: bool = True, out: Optional[torch.Tensor] = None,
+            fused: bool = False) -> torch.Tensor:
+        """Append (unless `append` is false) and attend; `fused` does both in the one
+        launch of dlfp_append_attention_mixed."""
         if out is None:
             out = torch.empty((self.batch.num_tokens, self.dims.num_q_heads, _d.HEAD_DIM),
                               dtype=out_dtype, device=self.device)
+        if fused:
+            if not append:
+                raise ValueError("the fused launch always appends")
+            self.batch.append_attention(self.pool, self.q, self.k_new, self.v_new, scale, out,
+                                        workspace)
+            return out
+        if append:
+            self.batch.append(self.pool, self.k_new, self.v_new)
         self.batch.attention(self.pool, self.q, scale, out, workspace)
         return out
 
@@ -174,7 +191,7 @@ class StagedBatch:
             _d._ptr32(kv_len), _d._ptr32(block_table), block_table.shape[1], int(num_blocks),
             ct.byref(m.c))
         _d._check(st, "dlfp_build_varlen_meta")
-        T, U = m.c.num_tokens, m.c.num_units
+        T, U = m.c.num_tokens, m.c.num_units + m.c.num_append
         h = self.host_np
         o = 0
         offs = []

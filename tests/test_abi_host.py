@@ -42,6 +42,8 @@ def _check_against_twin(dims, q_len, kv_len, bt, num_blocks, tuning=None):
     assert meta.slot_mapping[:meta.num_tokens].tolist() == slots
     om.check_work_list(meta.work, meta.num_prefill_units, q_len, kv_len, dims.num_q_heads,
                        dims.num_kv_heads, meta.num_groups, meta.workspace_bytes)
+    om.check_append_records(meta.append_records, meta.work, meta.num_prefill_units, q_len,
+                            kv_len, dims.num_kv_heads, meta.num_waiting_units)
     return meta
 
 

@@ -114,3 +114,50 @@ def test_checker_rejects_planted_defects(defect):
         work[3, om.W_QPOS0] -= 1
     with pytest.raises(om.WorkListError):
         om.check_work_list(work, npre, ql, kl, hq, hkv, ng, ws)
+
+
+def _append_records():
+    """Append records of the hand-built batch: seq 0's new tokens (positions
+    30..99) cut at page boundaries, one KV head; the decoder has none."""
+    runs = [(30, 2), (32, 16), (48, 16), (64, 16), (80, 16), (96, 4)]
+    recs = []
+    for pos, n in runs:
+        t0 = pos - _POS0[0]
+        r = _unit(0, 0, t0, n, pos, pos + n, kind=om.KIND_APPEND)
+        recs.append(r)
+    return np.stack(recs)
+
+
+def test_append_checker_accepts_valid_records():
+    work, npre, ql, kl, hq, hkv, ng, ws = _valid_list()
+    # every prefill unit's last key lies in page 1 or later (the first new token's page)
+    assert om.check_append_records(_append_records(), work, npre, ql, kl, hkv, 3) == {
+        "records": 6, "waiting": 3}
+
+
+@pytest.mark.parametrize("defect", ["drop", "dup", "cross", "decoder", "kind", "qrow",
+                                    "waiting"])
+def test_append_checker_rejects_planted_defects(defect):
+    work, npre, ql, kl, hq, hkv, ng, ws = _valid_list()
+    recs = _append_records()
+    waiting = 3
+    if defect == "drop":
+        recs = recs[1:]
+    elif defect == "dup":
+        recs = np.concatenate([recs, recs[2:3]])
+    elif defect == "cross":          # tokens 30..33 span pages 1 and 2
+        recs[0, om.W_QNTOK] = 4
+        recs[1, om.W_QTOK0] += 2
+        recs[1, om.W_QNTOK] -= 2
+        recs[1, om.W_QROW0] += 2
+        recs[1, om.W_QPOS0] += 2
+    elif defect == "decoder":
+        recs = np.concatenate([recs, _unit(1, 0, 0, 1, 39, 40, kind=om.KIND_APPEND)[None]])
+    elif defect == "kind":
+        recs[3, om.W_KIND] = om.KIND_PREFILL
+    elif defect == "qrow":
+        recs[4, om.W_QROW0] += 1
+    elif defect == "waiting":
+        waiting = 2
+    with pytest.raises(om.WorkListError):
+        om.check_append_records(recs, work, npre, ql, kl, hkv, waiting)
