@@ -343,7 +343,12 @@ def run_headline(args, dev, log_fn):
     latency = {}
     for p, s in stats.items():
         it = np.asarray(s["iter_ms"])
-        per_launch_ms = s["attn_ms"] / (s["recorded"] * cfg.layers)
+        n_l = s["recorded"] * cfg.layers
+        per_launch_ms = s["attn_ms"] / n_l
+        # whole-launch bounds from the algorithmic work of one call: ideal overlap of
+        # the HBM and MFMA shares (t_lb) and the two run back to back (t_sum)
+        t_b = s["bytes"] / n_l / (HBM_PEAK_GBS * 1e9)
+        t_f = s["flops"] / n_l / (MFMA_BF16_PEAK_TFLOPS * 1e12)
         latency[str(p)] = {
             "iter_ms_mean": round(float(it.mean()), 4), "iter_ms_p50": round(float(np.median(it)), 4),
             "iter_ms_p90": round(float(np.percentile(it, 90)), 4),
@@ -354,6 +359,8 @@ def run_headline(args, dev, log_fn):
             "iterations": len(it) // args.steps,
             "iterations_with_launch_events": s["recorded"] // args.steps,
             "controller_cap_last": s["caps"][-1],
+            "t_lb_us": round(max(t_b, t_f) * 1e6, 2), "t_sum_us": round((t_b + t_f) * 1e6, 2),
+            "t_lb_over_measured": round(max(t_b, t_f) / (per_launch_ms * 1e-3), 4),
         }
     avg_launch_s = attn_ms * 1e-3 / n_launch
     traffic = profiled_traffic()
@@ -519,22 +526,43 @@ def cpu_baseline(seconds):
              oa.bf16_bits_to_float64(s.v[:n])) for s, q, n in seqs]
     scale = 1.0 / math.sqrt(128)
     reps, t0 = 0, time.perf_counter()
+    t_pre = t_dec = 0.0
     while True:
-        for qq, kk, vv in data:
+        for i, (qq, kk, vv) in enumerate(data):
+            ts = time.perf_counter()
             oa.attention_sequence(qq, kk, vv, scale)
+            if i == 0:
+                t_pre += time.perf_counter() - ts
+            else:
+                t_dec += time.perf_counter() - ts
         reps += 1
         el = time.perf_counter() - t0
         if el >= seconds:
             break
     per_layer = el / reps
     tokens = p + cfg.n_decoders
-    threads = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
+    info = threadpool_info()
+    threads = max([d.get("num_threads", 1) for d in info] or [1])
+    blas = ", ".join(sorted({f"{d.get('internal_api')} {d.get('version')}" for d in info
+                             if d.get("user_api") == "blas"})) or "none loaded"
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
     return {"value": round(tokens / (per_layer * cfg.layers), 2), "unit": "tok/s",
             "cores": int(threads), "kind": "oracle",
             "sample": (f"float64 oracle, {reps} repetitions of one layer of one Qwen3-0.6B mixed "
                        f"iteration (p_t={p} at chunk {c}, 32 decoders), "
                        f"{per_layer * 1e3:.1f} ms per layer, scaled to 28 layers"),
-            "seconds": round(el, 2)}
+            "seconds": round(el, 2),
+            "prefill_ms_per_layer": round(t_pre * 1e3 / reps, 2),
+            "decode_ms_per_layer": round(t_dec * 1e3 / reps, 2),
+            "cpu_model": model, "nproc": os.cpu_count(), "blas": blas}
 
 
 # ----------------------------------------------------------------------------- main

@@ -65,7 +65,7 @@ extern "C" {
 #define DLFP_TILE_ROWS 128
 /* Longest key range of one work unit; the builder splits longer ranges.  A
  * unit keeps its slice of the block table in LDS, which bounds these. */
-#define DLFP_MAX_DECODE_UNIT_KEYS 8192
+#define DLFP_MAX_DECODE_UNIT_KEYS 4096
 #define DLFP_MAX_PREFILL_UNIT_KEYS 32768
 /* int32 fields per work unit (see dlfp_build_varlen_meta). */
 #define DLFP_WORK_INTS 16

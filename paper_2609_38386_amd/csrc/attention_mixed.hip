@@ -66,12 +66,16 @@ constexpr int PAGE_ELEMS = PAGE * D;          // bf16 elements per (block, head)
 constexpr int KV_TILE = 64;                   // keys per prefill tile (4 pages)
 constexpr int THREADS = 256;
 constexpr int PRE_PTAB = DLFP_MAX_PREFILL_UNIT_KEYS / PAGE;  // block ids of one prefill unit
-constexpr int LDS_BYTES = 4 * KV_TILE * D * 2 + PRE_PTAB * 4;  // 64 KiB of K/V tiles + 8 KiB
+constexpr int PRE_LDS = 4 * KV_TILE * D * 2 + PRE_PTAB * 4;  // 64 KiB of K/V tiles + 8 KiB
 constexpr int DEC_PTAB = DLFP_MAX_DECODE_UNIT_KEYS / PAGE;   // block ids of one decode unit
-// Per decode wave: K page, V page, probability buffer, block ids, and (for
-// g = 8) the query of the group.
+// Per decode wave: two slots of (K page, V page), probability buffer, block
+// ids, and (for g = 8) the query of the group.
 constexpr int DEC_Q_LDS = 8 * D * 2;
-constexpr int DEC_WAVE_LDS = 2 * PAGE_ELEMS * 2 + 16 * 16 * 2 + DEC_PTAB * 4 + DEC_Q_LDS;
+constexpr int DEC_PAGE_SLOT = 2 * PAGE_ELEMS * 2;  // K and V page, 8 KiB
+constexpr int DEC_WAVE_LDS = 2 * DEC_PAGE_SLOT + 16 * 16 * 2 + DEC_PTAB * 4 + DEC_Q_LDS;
+constexpr int LDS_BYTES = PRE_LDS > 4 * DEC_WAVE_LDS ? PRE_LDS : 4 * DEC_WAVE_LDS;
+// Two workgroups per CU (160 KiB of LDS).
+static_assert(2 * (LDS_BYTES + 16) <= 160 * 1024, "two workgroups must share a CU");
 constexpr float NEG_BIG = -1.0e30f;
 constexpr float LOG2E = 1.4426950408889634f;
 
@@ -809,9 +813,10 @@ __device__ void prefill_unit(const Args& a, const int32_t* it, char* smem, int* 
 
 // ---------------------------------------------------------------- decode
 
-// Wave-private LDS slice: K page (token rows, 16-byte chunk x of row R at
-// x ^ 8 (R & 1)), V^T page (64-byte dim-pair region r, 16-byte slot i at
-// (i + r / 4) & 3), then the probability buffer p[head][16 keys] in bf16.
+// Wave-private LDS slice: two page slots, each a K page (token rows, 16-byte
+// chunk x of row R at x ^ 8 (R & 1)) and a V^T page (64-byte dim-pair region
+// r, 16-byte slot i at (i + r / 4) & 3); then the probability buffer
+// p[head][16 keys] in bf16, the unit's block ids and (g = 8) the queries.
 template <int G, bool APP>
 __device__ void decode_unit(const Args& a, const int32_t* it, char* wl) {
   const int lane = threadIdx.x & 63;
@@ -821,19 +826,17 @@ __device__ void decode_unit(const Args& a, const int32_t* it, char* wl) {
   const int nsplits = uniform(it[DLFP_W_NSPLITS]);
   const int tok = uniform(it[DLFP_W_QROW0]);
   const int32_t* bt = a.block_table + (int64_t)s * a.max_blocks;
-  char* kl = wl;
-  char* vl = wl + PAGE_ELEMS * 2;
-  uint16_t* pbuf = reinterpret_cast<uint16_t*>(wl + 2 * PAGE_ELEMS * 2);
-  int32_t* ptab = reinterpret_cast<int32_t*>(wl + 2 * PAGE_ELEMS * 2 + 16 * 16 * 2);
+  uint16_t* pbuf = reinterpret_cast<uint16_t*>(wl + 2 * DEC_PAGE_SLOT);
+  int32_t* ptab = reinterpret_cast<int32_t*>(wl + 2 * DEC_PAGE_SLOT + 16 * 16 * 2);
 
   // Query of the g heads: lane uses dims [8c, 8c + 8) and [64 + 8c, 64 + 8c + 8).
   // Up to g = 4 they stay in registers; for g = 8 they live in the wave's LDS
-  // slice (each read is an 8-address broadcast) to leave registers for the
-  // page pipeline.
+  // slice (each read is an 8-address broadcast).
   constexpr bool Q_IN_LDS = G >= 8;
   constexpr int QR = Q_IN_LDS ? 1 : G;
   u32x4_t qa[QR], qb[QR];
-  uint16_t* qlds = reinterpret_cast<uint16_t*>(wl + 2 * PAGE_ELEMS * 2 + 16 * 16 * 2 + DEC_PTAB * 4);
+  uint16_t* qlds =
+      reinterpret_cast<uint16_t*>(wl + 2 * DEC_PAGE_SLOT + 16 * 16 * 2 + DEC_PTAB * 4);
   {
     const uint16_t* qp = a.q + ((int64_t)tok * a.hq + kh * G) * D;
     if constexpr (Q_IN_LDS) {
@@ -853,7 +856,7 @@ __device__ void decode_unit(const Args& a, const int32_t* it, char* wl) {
   // Append launches: the unit whose keys end with the sequence's new token
   // (position QPOS0) loads that token's key row (lanes 0-15, 16 bytes each)
   // and its values of dims 2 lane, 2 lane + 1, writes them to their slot, and
-  // puts them into the staged page in place of what the cache held there.
+  // puts them into the landed page in place of what the cache held there.
   const int newpos = uniform(it[DLFP_W_QPOS0]);
   const bool own_new = APP && newpos < ke;
   const int new_page = newpos / PAGE, new_off = newpos % PAGE;
@@ -886,47 +889,71 @@ __device__ void decode_unit(const Args& a, const int32_t* it, char* wl) {
     o1[h] = 0.f;
   }
 
-  // NSLOT register buffers rotate: while one page is consumed from LDS the
-  // next NSLOT are in flight.  One page (8 KiB) per wavefront is enough: the
-  // decode wavefronts of a launch then keep about 8 MB in flight, which
-  // saturates HBM, while more only lengthens the queues that the launch's
-  // prefill units wait in (measured on the Qwen3-0.6B sweep: 48.5-49.7 us per
-  // layer for chunks of 64-256 tokens with one page in flight, 51.9-52.8 us
-  // with two; the decode-only layer is unchanged).  The loop is
-  // straight-line: a page index past the unit's last page re-reads that page
-  // (an L2 hit) and every key in it is masked, and a block id outside the
-  // pool is replaced by block 0 after raising the error word, so the compiler
-  // can keep the prefetch in flight.
-  constexpr int NSLOT = 1;
-  u32x4_t fk[NSLOT][4], fv[NSLOT][4];
-  auto fetch = [&](u32x4_t* k4, u32x4_t* v4, int p) {
-    const int raw = ptab[min(p, p_end - 1) - p_begin];
+  // Page pipeline.  Pages reach the slot's LDS by direct global-to-LDS copies
+  // (no registers, no staging writes); each lane's source chunk is chosen so
+  // that the bytes land in the swizzled layout above.  Without a prefill share
+  // in the launch, page p + 2 is issued as soon as page p has been consumed,
+  // so one to two pages (8-16 KiB) per wavefront stay in flight (HBM delivers
+  // 6.0 TB/s to 8 wavefronts per CU with 8-16 KiB each in flight in a probe,
+  // 5.3 TB/s with 4 KiB).  Beside a prefill share, page p + 1 is issued when
+  // page p has landed, one page ahead: a deeper queue makes the prefill tiles
+  // wait longer for their loads (measured 3.6-5.5% longer iterations for
+  // chunks of 64-256 tokens).  A block id outside the pool is replaced by
+  // block 0 after raising the error word.
+  const bool deep = a.num_prefill == 0;
+  uint32_t kofs[4], vofs[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int ck = 64 * j + lane;  // LDS chunk this lane fills
+    const int R = ck >> 4, xs = ck & 15;
+    kofs[j] = R * 256 + ((xs ^ ((R & 1) << 3)) << 4);
+    const int rg = ck >> 2, si = ((ck & 3) - (rg >> 2)) & 3;
+    vofs[j] = (rg * 4 + si) * 16;
+  }
+  const uint32_t lds_wave = (uint32_t)uniform((int)lds_addr(wl));
+  auto issue = [&](int p, int slot) {
+    const int raw = ptab[p - p_begin];
     const bool ok = (unsigned)raw < (unsigned)a.num_blocks;
     if (!ok && lane == 0) raise_error(a.ws);
     const int64_t base = ((int64_t)(ok ? raw : 0) * a.hkv + kh) * PAGE_ELEMS;
+    const char* ksrc = reinterpret_cast<const char*>(a.kc + base);
+    const char* vsrc = reinterpret_cast<const char*>(a.vc + base);
+    const uint32_t dst = lds_wave + uniform(slot) * DEC_PAGE_SLOT;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      k4[j] = *reinterpret_cast<const u32x4_t*>(a.kc + base + (64 * j + lane) * 8);
-      v4[j] = *reinterpret_cast<const u32x4_t*>(a.vc + base + (64 * j + lane) * 8);
+      lds_copy16(ksrc + kofs[j], dst + j * 1024);
+      lds_copy16(vsrc + vofs[j], dst + PAGE_ELEMS * 2 + j * 1024);
     }
   };
+  // Vector-memory operations complete in issue order, so allowing the 8
+  // copies of the next page to stay outstanding waits for this one.
+  auto wait_page = [&](bool next_in_flight) {
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    if (next_in_flight)
+      __builtin_amdgcn_s_waitcnt(0x0F78);  // vmcnt(8)
+    else
+      __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  };
 
-  auto process = [&](u32x4_t* k4, u32x4_t* v4, int p) {
-    // Stage the fetched page in LDS, then refill the ring slot.
+  auto process = [&](int p, int slot) {
+    char* kl = wl + slot * DEC_PAGE_SLOT;
+    char* vl = kl + PAGE_ELEMS * 2;
+    wait_page(deep && p + 1 < p_end);
+    wave_sync();
+    if (!deep && p + 1 < p_end) issue(p + 1, slot ^ 1);  // that slot was consumed
+    if (p * PAGE + PAGE > ke) {
+      // Values past the unit's last key are zeroed (a probability of 0 times
+      // a NaN left in an unused slot would still be NaN).
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int q = 64 * j + lane;
-      const int R = q >> 4, x = q & 15;
-      *reinterpret_cast<u32x4_t*>(kl + R * 256 + ((x ^ ((R & 1) << 3)) << 4)) = k4[j];
-      const int rg = q >> 2, si = q & 3;
-      u32x4_t v = v4[j];
-      if (p * PAGE + PAGE > ke)
-        v = mask_elems(v, ke, [&](int e) { return p * PAGE + vt_pos(8 * (si & 1) + e); });
-      *reinterpret_cast<u32x4_t*>(vl + rg * 64 + (((si + (rg >> 2)) & 3) << 4)) = v;
+      for (int j = 0; j < 4; ++j) {
+        const int ck = 64 * j + lane;
+        const int rg = ck >> 2, si = ((ck & 3) - (rg >> 2)) & 3;
+        u32x4_t* v = reinterpret_cast<u32x4_t*>(vl + ck * 16);
+        *v = mask_elems(*v, ke, [&](int e) { return p * PAGE + vt_pos(8 * (si & 1) + e); });
+      }
     }
-    fetch(k4, v4, p + NSLOT);
     if (own_new && p == new_page) {
-      wave_sync();  // the staged copies land first
       if (lane < 16)
         *reinterpret_cast<u32x4_t*>(kl + new_off * 256 + ((lane ^ ((new_off & 1) << 3)) << 4)) = kn;
       // region lane holds dim 2 lane in slots 0-1 and dim 2 lane + 1 in slots 2-3
@@ -936,7 +963,7 @@ __device__ void decode_unit(const Args& a, const int32_t* it, char* wl) {
       *reinterpret_cast<uint16_t*>(v0) = (uint16_t)(vn & 0xFFFFu);
       *reinterpret_cast<uint16_t*>(v1) = (uint16_t)(vn >> 16);
     }
-    wave_sync();  // staged page visible to every lane
+    wave_sync();  // fixed-up page visible to every lane
 
     // Keys 8 st + kg of the page (st = 0, 1): each lane holds 16 dims of both.
     u32x4_t kv[2][2];
@@ -1017,14 +1044,15 @@ __device__ void decode_unit(const Args& a, const int32_t* it, char* wl) {
       o1[h] = a1;
       if constexpr (G >= 8) __builtin_amdgcn_sched_barrier(0);
     }
-    wave_sync();  // every lane done reading before the next page overwrites LDS
+    wave_sync();  // every lane done reading the slot before it is refilled
+    if (deep && p + 2 < p_end) issue(p + 2, slot);
   };
 
-#pragma unroll
-  for (int j = 0; j < NSLOT; ++j) fetch(fk[j], fv[j], p_begin + j);
-  for (int p = p_begin; p < p_end; p += NSLOT) {
-#pragma unroll
-    for (int j = 0; j < NSLOT; ++j) process(fk[j], fv[j], p + j);  // masked past p_end
+  issue(p_begin, 0);
+  if (deep && p_begin + 1 < p_end) issue(p_begin + 1, 1);
+  for (int p = p_begin; p < p_end; p += 2) {
+    process(p, 0);
+    if (p + 1 < p_end) process(p + 1, 1);
   }
 
   // Row sums live on the c == 0 lanes; total them.
