@@ -172,7 +172,9 @@ enum {
   DLFP_W_KIND = 11,    /* DLFP_KIND_PREFILL, DLFP_KIND_DECODE or DLFP_KIND_APPEND */
   DLFP_W_QROW0 = 12,   /* packed row of the unit's first token in q and out:
                           cu_q[seq] + QTOK0 */
-  DLFP_W_QPOS0 = 13    /* position of the unit's first token: q_pos0[seq] + QTOK0 */
+  DLFP_W_QPOS0 = 13,  /* position of the unit's first token: q_pos0[seq] + QTOK0 */
+  DLFP_W_PAGE0 = 14,  /* decode units: block id of the unit's first page (KVBEGIN / 16) */
+  DLFP_W_PAGE1 = 15   /* decode units: block id of its second page, -1 if it has one page */
 };
 enum { DLFP_KIND_PREFILL = 0, DLFP_KIND_DECODE = 1, DLFP_KIND_APPEND = 2 };
 
@@ -221,8 +223,9 @@ int dlfp_kv_append(const dlfp_dims* dims, int32_t num_tokens, const void* k_new,
  *
  * meta: the host metadata from dlfp_build_varlen_meta (only its counts are
  * read).  d_work, d_block_table: device copies of meta->work (each record
- * carries its sequence, rows, positions and key range) and of the block
- * table.  q, k_cache, v_cache: device bf16.  out: device,
+ * carries its sequence, rows, positions and key range; a decode unit's record
+ * also carries the block ids of its first two pages) and of the block table
+ * the metadata was built from.  q, k_cache, v_cache: device bf16.  out: device,
  * out_dtype 0 = bf16, 1 = fp32.  workspace: device scratch of at least
  * meta->workspace_bytes whose header and counter region (the first
  * DLFP_WORKSPACE_PARTIALS bytes) were zeroed once by dlfp_workspace_init;

@@ -169,6 +169,17 @@ __device__ __forceinline__ float sum_xor32(float x) {
 
 __device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
+// Work records are read-only for the launch: read through the constant
+// address space, so that a wave-uniform record comes in with scalar loads
+// (one round trip for all its fields).
+typedef const __attribute__((address_space(4))) int32_t* record_ptr;
+__device__ __forceinline__ record_ptr as_record(const int32_t* p) {
+  const uint64_t v = reinterpret_cast<uint64_t>(p);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return (record_ptr)(((uint64_t)hi << 32) | lo);
+}
+
 // Lanes of one wavefront hand data to each other through LDS.  The hardware
 // runs a wave's LDS operations in order; this keeps the compiler from moving a
 // lane's LDS accesses across the hand-off (it reasons per lane, so a store to
@@ -817,47 +828,112 @@ __device__ void prefill_unit(const Args& a, const int32_t* it, char* smem, int* 
 // chunk x of row R at x ^ 8 (R & 1)) and a V^T page (64-byte dim-pair region
 // r, 16-byte slot i at (i + r / 4) & 3); then the probability buffer
 // p[head][16 keys] in bf16, the unit's block ids and (g = 8) the queries.
+// Returns the next queue ticket's pending value when asked to take one (see
+// the kernel's decode loop): the ticket is taken a few pages before the unit
+// ends, so that its round trip overlaps the unit's last pages.
 template <int G, bool APP>
-__device__ void decode_unit(const Args& a, const int32_t* it, char* wl) {
+__device__ int decode_unit(const Args& a, const int32_t* it_g, char* wl, bool take_ticket) {
   const int lane = threadIdx.x & 63;
   const int kg = lane >> 3, c = lane & 7;
-  const int s = uniform(it[DLFP_W_SEQ]), kh = uniform(it[DLFP_W_KVHEAD]);
-  const int kb = uniform(it[DLFP_W_KVBEGIN]), ke = uniform(it[DLFP_W_KVEND]);
-  const int nsplits = uniform(it[DLFP_W_NSPLITS]);
-  const int tok = uniform(it[DLFP_W_QROW0]);
+  const record_ptr it = as_record(it_g);
+  const int s = it[DLFP_W_SEQ], kh = it[DLFP_W_KVHEAD];
+  const int kb = it[DLFP_W_KVBEGIN], ke = it[DLFP_W_KVEND];
+  const int nsplits = it[DLFP_W_NSPLITS];
+  const int tok = it[DLFP_W_QROW0];
+  const int newpos = it[DLFP_W_QPOS0];
+  const int first_blk = it[DLFP_W_PAGE0], second_blk = it[DLFP_W_PAGE1];
+  const int grp = it[DLFP_W_GROUP], wsgroup = it[DLFP_W_WSGROUP], split = it[DLFP_W_SPLIT];
   const int32_t* bt = a.block_table + (int64_t)s * a.max_blocks;
   uint16_t* pbuf = reinterpret_cast<uint16_t*>(wl + 2 * DEC_PAGE_SLOT);
   int32_t* ptab = reinterpret_cast<int32_t*>(wl + 2 * DEC_PAGE_SLOT + 16 * 16 * 2);
 
-  // Query of the g heads: lane uses dims [8c, 8c + 8) and [64 + 8c, 64 + 8c + 8).
-  // Up to g = 4 they stay in registers; for g = 8 they live in the wave's LDS
-  // slice (each read is an 8-address broadcast).
+  // Page pipeline.  Pages reach the slot's LDS by direct global-to-LDS copies
+  // (no registers, no staging writes); each lane's source chunk is chosen so
+  // that the bytes land in the swizzled layout above.  Without a prefill share
+  // in the launch, page p + 2 is issued as soon as page p has been consumed,
+  // so one to two pages (8-16 KiB) per wavefront stay in flight (HBM delivers
+  // 6.0 TB/s to 8 wavefronts per CU with 8-16 KiB each in flight in a probe,
+  // 5.3 TB/s with 4 KiB).  Beside a prefill share, page p + 1 is issued when
+  // page p has landed, one page ahead: a deeper queue makes the prefill tiles
+  // wait longer for their loads (measured 3.6-5.5% longer iterations for
+  // chunks of 64-256 tokens).  A block id outside the pool is replaced by
+  // block 0 after raising the error word.
+  const bool deep = a.num_prefill == 0;
+  const int p_begin = kb / PAGE, p_end = (ke + PAGE - 1) / PAGE;
+  const int npages = p_end - p_begin;
+  uint32_t kofs[4], vofs[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int ck = 64 * j + lane;  // LDS chunk this lane fills
+    const int R = ck >> 4, xs = ck & 15;
+    kofs[j] = R * 256 + ((xs ^ ((R & 1) << 3)) << 4);
+    const int rg = ck >> 2, si = ((ck & 3) - (rg >> 2)) & 3;
+    vofs[j] = (rg * 4 + si) * 16;
+  }
+  const uint32_t lds_wave = (uint32_t)uniform((int)lds_addr(wl));
+  auto issue_block = [&](int raw, int slot) {
+    const bool ok = (unsigned)raw < (unsigned)a.num_blocks;
+    if (!ok && lane == 0) raise_error(a.ws);
+    const int64_t base = ((int64_t)(ok ? raw : 0) * a.hkv + kh) * PAGE_ELEMS;
+    const char* ksrc = reinterpret_cast<const char*>(a.kc + base);
+    const char* vsrc = reinterpret_cast<const char*>(a.vc + base);
+    const uint32_t dst = lds_wave + uniform(slot) * DEC_PAGE_SLOT;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      lds_copy16(ksrc + kofs[j], dst + j * 1024);
+      lds_copy16(vsrc + vofs[j], dst + PAGE_ELEMS * 2 + j * 1024);
+    }
+  };
+  auto issue = [&](int p, int slot) { issue_block(uniform(ptab[p - p_begin]), slot); };
+  // Vector-memory operations complete in issue order, so allowing the 8
+  // copies of the next page to stay outstanding waits for this one.
+  auto wait_page = [&](bool next_in_flight) {
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    if (next_in_flight)
+      __builtin_amdgcn_s_waitcnt(0x0F78);  // vmcnt(8)
+    else
+      __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  };
+
+  // Prologue, one memory round trip after the work record: the first page
+  // (its block id comes with the record), the queries, the unit's block ids
+  // and (append launches) the new token's key and values all go out together,
+  // then the second page when two are kept in flight.  Queries of g <= 4 heads
+  // stay in registers (lane uses dims [8c, 8c + 8) and [64 + 8c, 64 + 8c + 8));
+  // for g = 8 they go to the wave's LDS slice (each read is an 8-address
+  // broadcast).  The append launch's unit whose keys end with the sequence's
+  // new token (position QPOS0) loads that token's key row (lanes 0-15, 16
+  // bytes each) and its values of dims 2 lane, 2 lane + 1, writes them to
+  // their slot, and puts them into the landed page in place of what the cache
+  // held there.
+  issue_block(first_blk, 0);
   constexpr bool Q_IN_LDS = G >= 8;
   constexpr int QR = Q_IN_LDS ? 1 : G;
   u32x4_t qa[QR], qb[QR];
   uint16_t* qlds =
       reinterpret_cast<uint16_t*>(wl + 2 * DEC_PAGE_SLOT + 16 * 16 * 2 + DEC_PTAB * 4);
-  {
-    const uint16_t* qp = a.q + ((int64_t)tok * a.hq + kh * G) * D;
-    if constexpr (Q_IN_LDS) {
+  const uint16_t* qp = a.q + ((int64_t)tok * a.hq + kh * G) * D;
+  constexpr int QCH = Q_IN_LDS ? G * D / 8 / 64 : 1;  // 16-byte query chunks per lane (g = 8)
+  u32x4_t qv[QCH];
+  if constexpr (Q_IN_LDS) {
 #pragma unroll
-      for (int i = lane; i < G * D / 8; i += 64)
-        *reinterpret_cast<u32x4_t*>(qlds + 8 * i) = *reinterpret_cast<const u32x4_t*>(qp + 8 * i);
-    } else {
+    for (int k = 0; k < QCH; ++k)
+      qv[k] = *reinterpret_cast<const u32x4_t*>(qp + 8 * (lane + 64 * k));
+  } else {
 #pragma unroll
-      for (int h = 0; h < G; ++h) {
-        qa[h] = *reinterpret_cast<const u32x4_t*>(qp + h * D + 8 * c);
-        qb[h] = *reinterpret_cast<const u32x4_t*>(qp + h * D + 64 + 8 * c);
-      }
+    for (int h = 0; h < G; ++h) {
+      qa[h] = *reinterpret_cast<const u32x4_t*>(qp + h * D + 8 * c);
+      qb[h] = *reinterpret_cast<const u32x4_t*>(qp + h * D + 64 + 8 * c);
     }
   }
-  const int p_begin = kb / PAGE, p_end = (ke + PAGE - 1) / PAGE;
-  for (int i = lane; i < p_end - p_begin; i += 64) ptab[i] = bt[p_begin + i];
-  // Append launches: the unit whose keys end with the sequence's new token
-  // (position QPOS0) loads that token's key row (lanes 0-15, 16 bytes each)
-  // and its values of dims 2 lane, 2 lane + 1, writes them to their slot, and
-  // puts them into the landed page in place of what the cache held there.
-  const int newpos = uniform(it[DLFP_W_QPOS0]);
+  constexpr int PTV = DEC_PTAB / 64;
+  int ptv[PTV];
+#pragma unroll
+  for (int k = 0; k < PTV; ++k) {
+    const int i = lane + 64 * k;
+    ptv[k] = i < npages ? bt[p_begin + i] : 0;
+  }
   const bool own_new = APP && newpos < ke;
   const int new_page = newpos / PAGE, new_off = newpos % PAGE;
   u32x4_t kn = {0u, 0u, 0u, 0u};
@@ -867,7 +943,15 @@ __device__ void decode_unit(const Args& a, const int32_t* it, char* wl) {
     if (lane < 16) kn = *reinterpret_cast<const u32x4_t*>(a.k_new + src + 8 * lane);
     vn = *reinterpret_cast<const uint32_t*>(a.v_new + src + 2 * lane);
   }
-  wait_memory_complete();  // queries and block ids resident before the page pipeline starts
+  if (deep && npages > 1) issue_block(second_blk, 1);
+  wait_memory_complete();  // everything above has landed
+  if constexpr (Q_IN_LDS) {
+#pragma unroll
+    for (int k = 0; k < QCH; ++k) *reinterpret_cast<u32x4_t*>(qlds + 8 * (lane + 64 * k)) = qv[k];
+  }
+#pragma unroll
+  for (int k = 0; k < PTV; ++k)
+    if (lane + 64 * k < npages) ptab[lane + 64 * k] = ptv[k];
   wave_sync();
   if (own_new) {
     const int raw = ptab[new_page - p_begin];
@@ -888,53 +972,9 @@ __device__ void decode_unit(const Args& a, const int32_t* it, char* wl) {
     o0[h] = 0.f;
     o1[h] = 0.f;
   }
-
-  // Page pipeline.  Pages reach the slot's LDS by direct global-to-LDS copies
-  // (no registers, no staging writes); each lane's source chunk is chosen so
-  // that the bytes land in the swizzled layout above.  Without a prefill share
-  // in the launch, page p + 2 is issued as soon as page p has been consumed,
-  // so one to two pages (8-16 KiB) per wavefront stay in flight (HBM delivers
-  // 6.0 TB/s to 8 wavefronts per CU with 8-16 KiB each in flight in a probe,
-  // 5.3 TB/s with 4 KiB).  Beside a prefill share, page p + 1 is issued when
-  // page p has landed, one page ahead: a deeper queue makes the prefill tiles
-  // wait longer for their loads (measured 3.6-5.5% longer iterations for
-  // chunks of 64-256 tokens).  A block id outside the pool is replaced by
-  // block 0 after raising the error word.
-  const bool deep = a.num_prefill == 0;
-  uint32_t kofs[4], vofs[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int ck = 64 * j + lane;  // LDS chunk this lane fills
-    const int R = ck >> 4, xs = ck & 15;
-    kofs[j] = R * 256 + ((xs ^ ((R & 1) << 3)) << 4);
-    const int rg = ck >> 2, si = ((ck & 3) - (rg >> 2)) & 3;
-    vofs[j] = (rg * 4 + si) * 16;
-  }
-  const uint32_t lds_wave = (uint32_t)uniform((int)lds_addr(wl));
-  auto issue = [&](int p, int slot) {
-    const int raw = ptab[p - p_begin];
-    const bool ok = (unsigned)raw < (unsigned)a.num_blocks;
-    if (!ok && lane == 0) raise_error(a.ws);
-    const int64_t base = ((int64_t)(ok ? raw : 0) * a.hkv + kh) * PAGE_ELEMS;
-    const char* ksrc = reinterpret_cast<const char*>(a.kc + base);
-    const char* vsrc = reinterpret_cast<const char*>(a.vc + base);
-    const uint32_t dst = lds_wave + uniform(slot) * DEC_PAGE_SLOT;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      lds_copy16(ksrc + kofs[j], dst + j * 1024);
-      lds_copy16(vsrc + vofs[j], dst + PAGE_ELEMS * 2 + j * 1024);
-    }
-  };
-  // Vector-memory operations complete in issue order, so allowing the 8
-  // copies of the next page to stay outstanding waits for this one.
-  auto wait_page = [&](bool next_in_flight) {
-    __atomic_signal_fence(__ATOMIC_SEQ_CST);
-    if (next_in_flight)
-      __builtin_amdgcn_s_waitcnt(0x0F78);  // vmcnt(8)
-    else
-      __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
-    __atomic_signal_fence(__ATOMIC_SEQ_CST);
-  };
+  // Queue mode: the next ticket is taken a few pages before the unit ends.
+  int ticket_v = 0;
+  const int ticket_page = max(p_begin, p_end - 4);
 
   auto process = [&](int p, int slot) {
     char* kl = wl + slot * DEC_PAGE_SLOT;
@@ -942,6 +982,9 @@ __device__ void decode_unit(const Args& a, const int32_t* it, char* wl) {
     wait_page(deep && p + 1 < p_end);
     wave_sync();
     if (!deep && p + 1 < p_end) issue(p + 1, slot ^ 1);  // that slot was consumed
+    if (take_ticket && p == ticket_page && lane == 0)
+      ticket_v = __hip_atomic_fetch_add(header_word(a.ws, HDR_TICKET), 1, __ATOMIC_RELAXED,
+                                        __HIP_MEMORY_SCOPE_AGENT);
     if (p * PAGE + PAGE > ke) {
       // Values past the unit's last key are zeroed (a probability of 0 times
       // a NaN left in an unused slot would still be NaN).
@@ -1048,8 +1091,6 @@ __device__ void decode_unit(const Args& a, const int32_t* it, char* wl) {
     if (deep && p + 2 < p_end) issue(p + 2, slot);
   };
 
-  issue(p_begin, 0);
-  if (deep && p_begin + 1 < p_end) issue(p_begin + 1, 1);
   for (int p = p_begin; p < p_end; p += 2) {
     process(p, 0);
     if (p + 1 < p_end) process(p + 1, 1);
@@ -1072,13 +1113,13 @@ __device__ void decode_unit(const Args& a, const int32_t* it, char* wl) {
       const float inv = 1.f / l[h];
       store2(a, obase + h * D, o0[h] * inv, o1[h] * inv);
     }
-    return;
+    return ticket_v;
   }
 
   // Partial: O[G][128], m[G], l[G].
   const int slot_floats = slot_floats_for(G);
-  const Slots sl = group_slots(a.ws, uniform(it[DLFP_W_WSGROUP]), nsplits, slot_floats);
-  const int my = uniform(it[DLFP_W_SPLIT]) * slot_floats;
+  const Slots sl = group_slots(a.ws, wsgroup, nsplits, slot_floats);
+  const int my = split * slot_floats;
 #pragma unroll
   for (int h = 0; h < G; ++h) {
     pstore2(sl, my + h * D + 2 * lane, f32x2_t{o0[h], o1[h]});
@@ -1087,12 +1128,11 @@ __device__ void decode_unit(const Args& a, const int32_t* it, char* wl) {
       pstore1(sl, my + G * D + G + h, l[h]);
     }
   }
-  const int grp = uniform(it[DLFP_W_GROUP]);
   wait_memory_complete();
   int old = 0;
   if (lane == 0) old = arrive(a.ws, grp);
   old = __shfl(old, 0);
-  if (old != nsplits - 1) return;
+  if (old != nsplits - 1) return ticket_v;
 
   // Last arriver.  Entry f = j G + h stands for head h of split j.  Per batch
   // of up to 64 entries, lane e loads entry e's maximum and row sum while
@@ -1167,6 +1207,7 @@ __device__ void decode_unit(const Args& a, const int32_t* it, char* wl) {
   }
   if (lane == 0)
     __hip_atomic_store(group_counter(a.ws, grp), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return ticket_v;
 }
 
 // ---------------------------------------------------------------- append
@@ -1306,10 +1347,12 @@ __global__ __launch_bounds__(THREADS, 2) void attention_mixed_kernel(Args a) {
     int t = (b - a.num_prefill) * 4 + wave;
     if (queue && t >= a.decode_static) t = ticket();
     while (t < ndec) {
-      decode_unit<G, APP>(a, a.work + (int64_t)(a.num_prefill + t) * DLFP_WORK_INTS, wl);
+      // In queue mode the unit takes the next ticket itself near its end.
+      const int pending = decode_unit<G, APP>(
+          a, a.work + (int64_t)(a.num_prefill + t) * DLFP_WORK_INTS, wl, queue);
       wave_sync();
       if (!queue) break;
-      t = ticket();
+      t = a.decode_static + uniform(__shfl(pending, 0));
     }
     if (queue) {
       __syncthreads();

@@ -292,6 +292,15 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
       u.f[DLFP_W_KIND] = kind;
       u.f[DLFP_W_QROW0] = (int32_t)(cu_q_of[s] + t0);
       u.f[DLFP_W_QPOS0] = (int32_t)(kv_len[s] - q_len[s] + t0);
+      if (kind == DLFP_KIND_DECODE) {
+        // The unit's first two block ids travel with the record, so its first
+        // page loads go out with its query and block-table loads.
+        const int32_t* row = block_table + (int64_t)s * max_blocks;
+        const int64_t pg = u.f[DLFP_W_KVBEGIN] / DLFP_PAGE_SIZE;
+        const int64_t last = (u.f[DLFP_W_KVEND] - 1) / DLFP_PAGE_SIZE;
+        u.f[DLFP_W_PAGE0] = row[pg];
+        u.f[DLFP_W_PAGE1] = pg + 1 <= last ? row[pg + 1] : -1;
+      }
       units.push_back(u);
     }
   };

@@ -44,6 +44,13 @@ def _check_against_twin(dims, q_len, kv_len, bt, num_blocks, tuning=None):
                        dims.num_kv_heads, meta.num_groups, meta.workspace_bytes)
     om.check_append_records(meta.append_records, meta.work, meta.num_prefill_units, q_len,
                             kv_len, dims.num_kv_heads, meta.num_waiting_units)
+    # decode units carry the block ids of their first two pages
+    bt = np.asarray(bt)
+    for u in meta.work[meta.num_prefill_units:]:
+        s, kb, ke = int(u[0]), int(u[4]), int(u[5])
+        pg = kb // 16
+        assert u[14] == bt[s][pg]
+        assert u[15] == (bt[s][pg + 1] if (ke - 1) // 16 >= pg + 1 else -1)
     return meta
 
 

@@ -214,10 +214,18 @@ def test_bad_block_id_raises_error_word_without_reading(dev):
     it = rt.Iteration(D.make_dims(16, 8), seqs, 8, 2, dev)
     ws2 = rt.Workspace(dev, 1 << 16)
     bad = it.batch.d_block_table.clone()
-    bad[0, 1] = 10_000
+    bad[0, 2] = 10_000   # the first two pages' ids travel with the work record
     it.batch.d_block_table = bad
     it.run(ws2, SCALE, torch.float32, append=False)
     assert D.dlfp_workspace_error(ws2.buf) == 1
+    # a bad id in a decode record's second-page field is caught the same way
+    it2 = rt.Iteration(D.make_dims(16, 8), seqs, 8, 2, dev)
+    ws3 = rt.Workspace(dev, 1 << 16)
+    w = it2.batch.d_work.clone()
+    w[3 * D.WORK_INTS + 15] = 10_000
+    it2.batch.d_work = w
+    it2.run(ws3, SCALE, torch.float32, append=False)
+    assert D.dlfp_workspace_error(ws3.buf) == 1
 
 
 def test_abi_rejects_bad_arguments(dev, ws):
