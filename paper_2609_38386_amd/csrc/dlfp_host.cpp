@@ -270,11 +270,27 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
   std::vector<int64_t> group_rows;  // rows of each group
   // A key range longer than the split is cut into equal parts (rounded up
   // to the granule), so the units of a group finish together.
+  // With `tail`, the last part is cut again into a half and two quarters
+  // (decode units that run in several queue rounds: the queue hands out the
+  // longest units first, so these short pieces even out the end of the launch).
+  std::vector<int64_t> cut;
   auto emit = [&](int s, int kh, int64_t t0, int64_t nt, int64_t kend, int64_t split,
-                  int64_t granule, int kind) {
+                  int64_t granule, int kind, bool tail = false) {
     int64_t nsp = ceil_div(kend, split);
     const int64_t part = round_up(ceil_div(kend, nsp), granule);
     nsp = ceil_div(kend, part);
+    cut.clear();
+    for (int64_t j = 0; j < nsp; ++j) cut.push_back(j * part);
+    if (tail) {
+      const int64_t b = (nsp - 1) * part, len = kend - b;
+      const int64_t h = round_up(ceil_div(len, 2), granule), q = round_up(ceil_div(len - h, 2), granule);
+      if (len >= 4 * granule && h < len && h + q < len) {
+        cut.push_back(b + h);
+        cut.push_back(b + h + q);
+      }
+    }
+    cut.push_back(kend);
+    nsp = (int64_t)cut.size() - 1;
     const int32_t grp = nsp > 1 ? groups++ : -1;
     if (nsp > 1) group_rows.push_back(nt * g);
     for (int64_t j = 0; j < nsp; ++j) {
@@ -284,8 +300,8 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
       u.f[DLFP_W_KVHEAD] = kh;
       u.f[DLFP_W_QTOK0] = (int32_t)t0;
       u.f[DLFP_W_QNTOK] = (int32_t)nt;
-      u.f[DLFP_W_KVBEGIN] = (int32_t)(j * part);
-      u.f[DLFP_W_KVEND] = (int32_t)std::min(kend, (j + 1) * part);
+      u.f[DLFP_W_KVBEGIN] = (int32_t)cut[j];
+      u.f[DLFP_W_KVEND] = (int32_t)cut[j + 1];
       u.f[DLFP_W_GROUP] = grp;
       u.f[DLFP_W_SPLIT] = (int32_t)j;
       u.f[DLFP_W_NSPLITS] = (int32_t)nsp;
@@ -328,10 +344,22 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
       emit(t.s, kh, t.t0, t.nt, t.kend, split_p, KV_GRANULE_PREFILL, DLFP_KIND_PREFILL);
   }
   const int64_t num_prefill = (int64_t)units.size();
+  // Decode units that run in a few queue rounds (more units than the wavefronts
+  // the prefill units leave, but not so many that the last round is a small
+  // part of the launch anyway) get the short tail pieces.
+  bool decode_tail = false;
+  if (!tn.decode_split_tokens) {
+    int64_t n_dec = 0;
+    for (int s = 0; s < num_seqs; ++s)
+      if (q_len[s] == 1) n_dec += hkv * ceil_div(kv_len[s], split_d);
+    const int64_t slots_d = num_prefill < resident / 4
+                                ? std::max<int64_t>(resident / 4 - num_prefill, 64) : resident / 4;
+    decode_tail = n_dec > 4 * slots_d && n_dec <= 24 * slots_d;
+  }
   for (int s = 0; s < num_seqs; ++s) {
     if (q_len[s] != 1) continue;
     for (int kh = 0; kh < hkv; ++kh)
-      emit(s, kh, 0, 1, kv_len[s], split_d, DLFP_PAGE_SIZE, DLFP_KIND_DECODE);
+      emit(s, kh, 0, 1, kv_len[s], split_d, DLFP_PAGE_SIZE, DLFP_KIND_DECODE, decode_tail);
   }
   // Decode wavefronts take units in list order from a queue: longest first.
   std::stable_sort(units.begin() + num_prefill, units.end(), [](const Unit& x, const Unit& y) {

@@ -128,6 +128,30 @@ def test_meta_small_prefill_share_takes_latency_tiles():
     assert meta.work[:meta.num_prefill_units, 3].max() == 64
 
 
+def test_meta_decode_tail_pieces_in_a_few_queue_rounds():
+    # Qwen3-8B decoders alone (32 query / 8 KV heads): several queue rounds of
+    # decode units, so each (sequence, KV head) range ends in a half and two
+    # quarters of its last split part
+    cfg = wl.qwen3_8b_config()
+    pages = cfg.pages_per_seq()
+    bt = wl.block_tables(cfg.seed, pages, int(sum(pages)))[:cfg.n_decoders]
+    kv = [int(c) for c in cfg.decoder_contexts()]
+    dims = D.make_dims(cfg.shape.num_q_heads, cfg.shape.num_kv_heads)
+    meta = _check_against_twin(dims, [1] * len(kv), kv, bt, int(sum(pages)))
+    split = meta.decode_split_tokens
+    plain = sum(cfg.shape.num_kv_heads * math.ceil(k / split) for k in kv)
+    assert meta.num_units > plain
+    w = meta.work
+    for s in range(3):
+        rows = w[(w[:, 0] == s) & (w[:, 1] == 0)]
+        rows = rows[np.argsort(rows[:, 4])]
+        lens = rows[:, 5] - rows[:, 4]
+        last = lens[-3:].sum()
+        if last >= 64:
+            assert lens[-3] >= lens[-2] >= lens[-1] and lens[-3] >= last // 2, lens
+        assert (rows[:-3, 5] - rows[:-3, 4] == (rows[0, 5] - rows[0, 4])).all()
+
+
 def test_meta_empty_batch():
     meta = D.dlfp_build_varlen_meta(D.make_dims(16, 8), [], [], np.zeros((0, 1), np.int32), 4)
     assert meta.num_seqs == 0 and meta.num_units == 0 and meta.workspace_bytes >= 256
