@@ -508,6 +508,35 @@ def run_replays(dev, seeds, log_fn):
     return out
 
 
+def run_overlap_replay(dev, seed, rate, log_fn):
+    """The same replay at a higher arrival rate, so that prompts arrive while
+    others decode for most of the run: the controller's steady state (L/T on the
+    guarded cycles whose cap came from a feedback update), uncapped vs DLFP."""
+    from paper_2609_38386_amd import replay as rp
+    keys = ("itl_p50_ms", "itl_p99_ms", "ttft_p50_ms", "ttft_p99_ms", "iterations",
+            "guarded_iterations", "controlled_iterations", "controlled_L_over_T_mean",
+            "controlled_L_over_T_p50", "controlled_L_over_T_p90", "controlled_within_target",
+            "controlled_within_5pct", "reconciled")
+    cfg = rp.ReplayConfig(seed=seed, rate_per_s=rate)
+    ex = rp.GpuExecutor(cfg, dev)
+    trace = []
+    t0 = time.time()
+    base = rp.run_replay(cfg, rp.Policy(rp.Policy.UNCAPPED), ex, trace=trace)
+    target = 1.2 * float(np.median([it["layer_ms"] for it in trace
+                                    if it["decoders"] > 0 and it["p_t"] == 0]))
+    trace = []
+    dl = rp.run_replay(cfg, rp.Policy(rp.Policy.DLFP, target_ms=target, cfg=cfg), ex, trace=trace)
+    caps = [it["limit"] for it in trace if it["guarded"]]
+    out = {"seed": seed, "rate_per_s": rate, "target_layer_ms": round(target, 5),
+           "guarded_cap_p50": int(np.median(caps)) if caps else None}
+    for name, r in (("uncapped", base), ("dlfp", dl)):
+        out[name] = {k: (round(r[k], 4) if isinstance(r[k], float) else r[k]) for k in keys}
+    log_fn(f"overlap replay {rate} req/s: {time.time() - t0:.1f}s, controlled L/T p50 "
+           f"{dl['controlled_L_over_T_p50']}, within 5% {dl['controlled_within_5pct']}")
+    del ex
+    return out
+
+
 # ----------------------------------------------------------------------------- CPU baseline
 
 def cpu_baseline(seconds):
@@ -624,7 +653,9 @@ def main():
         logf(f"{name} done")
     replay = None
     if args.replay_seeds not in ("", "none"):
-        replay = run_replays(dev, [int(x) for x in args.replay_seeds.split(",")], logf)
+        seeds = [int(x) for x in args.replay_seeds.split(",")]
+        replay = run_replays(dev, seeds, logf)
+        replay["overlap_20_req_s"] = run_overlap_replay(dev, seeds[0], 20.0, logf)
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(args.cpu_seconds)

@@ -248,6 +248,12 @@ def run_replay(cfg: ReplayConfig, policy: Policy, execute: Executor,
         "controlled_L_over_T_mean": float(np.mean(controlled_ratio)) if controlled_ratio else None,
         "controlled_within_target": (float(np.mean(np.asarray(controlled_ratio) <= 1.0))
                                      if controlled_ratio else None),
+        "controlled_within_5pct": (float(np.mean(np.asarray(controlled_ratio) <= 1.05))
+                                   if controlled_ratio else None),
+        "controlled_L_over_T_p50": (float(np.percentile(controlled_ratio, 50))
+                                    if controlled_ratio else None),
+        "controlled_L_over_T_p90": (float(np.percentile(controlled_ratio, 90))
+                                    if controlled_ratio else None),
         "reconciled": reconciled,
         "prompt_tokens": int(sum(r.prompt_len for r in reqs)),
         "output_tokens": int(sum(r.generated for r in reqs)),

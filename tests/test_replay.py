@@ -103,5 +103,7 @@ def test_controlled_cycles_hold_a_reachable_target():
     assert 0.8 <= r["controlled_L_over_T_mean"] <= 1.1
     assert r["controlled_within_target"] >= 0.5
     assert r["guarded_L_over_T_mean"] >= r["controlled_L_over_T_mean"]
+    assert r["controlled_within_5pct"] >= r["controlled_within_target"]
+    assert r["controlled_L_over_T_p50"] <= r["controlled_L_over_T_p90"]
     base = rp.run_replay(cfg, rp.Policy(rp.Policy.UNCAPPED), model)
     assert base["controlled_iterations"] == 0 and base["controlled_L_over_T_mean"] is None
