@@ -380,40 +380,54 @@ def run_headline(args, dev, log_fn):
     return cfg, result
 
 
-def measure_shares(sw, cfg, reps=2):
-    """Decode-only and prefill-only launches of the same kernel (rotating pools)."""
+def measure_shares(sw, cfg, min_launches=20):
+    """Decode-only and prefill-only launches of the same kernel (rotating pools),
+    at least ``min_launches`` of each, each timed with its own events.  Rates are
+    the median over launches of algorithmic work / launch time; the 90th
+    percentile of the launch time is reported beside the median."""
+    reps = max(1, -(-min_launches // sw.layers))
+
+    def summary(times_ms, work):
+        t = np.asarray(times_ms)
+        rate = np.asarray(work) / (t * 1e-3)
+        return t, float(np.median(rate))
+
     out = {}
-    attn, b, f = 0.0, 0, 0
+    times, work = [], []
     for r in range(reps):
         _, a, ql, kl = sw.iteration(cfg.chunks[0], r, prefill=False)
-        attn += sum(a)
-        db, _, df, _ = attn_work(sw.hq, sw.hkv, ql, kl)
+        db, _, _, _ = attn_work(sw.hq, sw.hkv, ql, kl)
         db += append_work(sw.hkv, int(ql.sum())) if sw.fused else 0
-        b += db * sw.layers
-        f += df * sw.layers
-    gbs = b / (attn * 1e-3) / 1e9
+        times += list(a)
+        work += [db] * len(a)
+    t, rate = summary(times, work)
+    gbs = rate / 1e9
     out["decode"] = {"GBps": round(gbs, 1), "frac_hbm": round(gbs / HBM_PEAK_GBS, 4),
-                     "us_per_layer": round(attn * 1e3 / (reps * sw.layers), 2),
-                     "bytes_per_layer": int(b / (reps * sw.layers))}
+                     "us_per_layer": round(float(np.median(t)) * 1e3, 2),
+                     "us_p90": round(float(np.percentile(t, 90)) * 1e3, 2),
+                     "launches": len(t), "bytes_per_layer": int(np.median(work))}
     pre = {}
     for p in cfg.chunks:
         c = cfg.prompt_len // p - 1
-        attn, b, f = 0.0, 0, 0
+        times, fl, by = [], [], []
         for r in range(reps):
             _, a, ql, kl = sw.iteration(p, c, decoders=False)
-            attn += sum(a)
             _, pb, _, pf = attn_work(sw.hq, sw.hkv, ql, kl)
             pb += append_work(sw.hkv, int(ql.sum())) if sw.fused else 0
-            b += pb * sw.layers
-            f += pf * sw.layers
-        sec = attn * 1e-3
-        tf = f / sec / 1e12
+            times += list(a)
+            fl += [pf] * len(a)
+            by += [pb] * len(a)
+        t, tf = summary(times, fl)
+        _, bs = summary(times, by)
+        tf /= 1e12
         g = sw.hq // sw.hkv
         pre[str(p)] = {"TFLOPs": round(tf, 1), "frac_mfma": round(tf / MFMA_BF16_PEAK_TFLOPS, 4),
-                       "GBps": round(b / sec / 1e9, 1),
-                       "frac_hbm": round(b / sec / 1e9 / HBM_PEAK_GBS, 4),
+                       "GBps": round(bs / 1e9, 1),
+                       "frac_hbm": round(bs / 1e9 / HBM_PEAK_GBS, 4),
                        "above_ridge": bool(g * p >= 315),
-                       "us_per_layer": round(attn * 1e3 / (reps * sw.layers), 2)}
+                       "us_per_layer": round(float(np.median(t)) * 1e3, 2),
+                       "us_p90": round(float(np.percentile(t, 90)) * 1e3, 2),
+                       "launches": len(t)}
     out["prefill_last_chunk"] = pre
     return out
 
@@ -447,7 +461,7 @@ def run_extra(name, dev, log_fn, fused=True):
                        "model_iter_ms_mean": round(float(np.mean(ms_l)) * cfg.layers, 3),
                        "attn_GBps": round(b_l / sec / 1e9, 1),
                        "attn_TFLOPs": round(f_l / sec / 1e12, 1)}
-    shares = measure_shares(sw, cfg, reps=1)
+    shares = measure_shares(sw, cfg)
     del sw
     torch.cuda.empty_cache()
     return {"shape": f"Hq{cfg.shape.num_q_heads}/Hkv{cfg.shape.num_kv_heads}/d128",
