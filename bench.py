@@ -525,7 +525,9 @@ def run_replays(dev, seeds, log_fn):
 def run_overlap_replay(dev, seed, rate, log_fn):
     """The same replay at a higher arrival rate, so that prompts arrive while
     others decode for most of the run: the controller's steady state (L/T on the
-    guarded cycles whose cap came from a feedback update), uncapped vs DLFP."""
+    guarded cycles whose cap came from a feedback update), uncapped vs DLFP, and
+    DLFP fed each completion time one iteration late (what an asynchronous
+    engine that sets the next cap while the current iteration runs observes)."""
     from paper_2609_38386_amd import replay as rp
     keys = ("itl_p50_ms", "itl_p99_ms", "ttft_p50_ms", "ttft_p99_ms", "iterations",
             "guarded_iterations", "controlled_iterations", "controlled_L_over_T_mean",
@@ -541,9 +543,10 @@ def run_overlap_replay(dev, seed, rate, log_fn):
     trace = []
     dl = rp.run_replay(cfg, rp.Policy(rp.Policy.DLFP, target_ms=target, cfg=cfg), ex, trace=trace)
     caps = [it["limit"] for it in trace if it["guarded"]]
+    lag = rp.run_replay(cfg, rp.Policy(rp.Policy.DLFP_LAG1, target_ms=target, cfg=cfg), ex)
     out = {"seed": seed, "rate_per_s": rate, "target_layer_ms": round(target, 5),
            "guarded_cap_p50": int(np.median(caps)) if caps else None}
-    for name, r in (("uncapped", base), ("dlfp", dl)):
+    for name, r in (("uncapped", base), ("dlfp", dl), ("dlfp_lag1", lag)):
         out[name] = {k: (round(r[k], 4) if isinstance(r[k], float) else r[k]) for k in keys}
     log_fn(f"overlap replay {rate} req/s: {time.time() - t0:.1f}s, controlled L/T p50 "
            f"{dl['controlled_L_over_T_p50']}, within 5% {dl['controlled_within_5pct']}")

@@ -113,13 +113,18 @@ class Policy:
     UNCAPPED = "uncapped"
     FIXED = "fixed"
     DLFP = "dlfp"
+    # Eq. 2 fed one iteration late: an asynchronous engine that sets the cap of
+    # iteration t + 1 while iteration t still runs only has the completion time
+    # of iteration t - 1 (the stale signal of Sec. 6.4).
+    DLFP_LAG1 = "dlfp_lag1"
 
     def __init__(self, kind: str, cap: int = 0, target_ms: float = 0.0, cfg: ReplayConfig = None):
         self.kind = kind
         self.fixed_cap = cap
         self.target_ms = target_ms
         self.ctrl = None
-        if kind == self.DLFP:
+        self.pending = None       # DLFP_LAG1: the observation not yet delivered
+        if kind in (self.DLFP, self.DLFP_LAG1):
             from . import dlfp as D
             self._D = D
             self.ctrl = D.dlfp_controller_init(target_ms, cfg.c_initial, cfg.c_min, cfg.c_max,
@@ -138,7 +143,12 @@ class Policy:
         return min(cap, budget)
 
     def observe(self, n_decoding_next: int, guarded: bool, observed_ms: float):
-        if self.kind == self.DLFP:
+        if self.kind == self.DLFP_LAG1:
+            # this iteration's completion is delivered one call later; the
+            # previous one's arrives now (nothing before the first completion)
+            prev, self.pending = self.pending, (guarded, observed_ms)
+            guarded, observed_ms = prev if prev is not None else (False, observed_ms)
+        if self.kind in (self.DLFP, self.DLFP_LAG1):
             if guarded:
                 self.controlled = True
             elif n_decoding_next == 0:
