@@ -53,7 +53,8 @@ def parse_args():
     ap.add_argument("--two-launch", action="store_true",
                     help="append with dlfp_kv_append, then dlfp_attention_mixed (instead of "
                          "the one-launch dlfp_append_attention_mixed)")
-    ap.add_argument("--pmc-workload", choices=["sweep", "shares"], default=None,
+    ap.add_argument("--pmc-workload", choices=["sweep", "shares", "shares-8b", "shares-32b"],
+                    default=None,
                     help="counter-pass workloads: 'sweep' = one headline sweep plus a 1 GiB "
                          "device copy; 'shares' = decode-only and prefill-only launches")
     return ap.parse_args()
@@ -617,9 +618,22 @@ def pmc_workload(dev, kind, fused=True):
     """'sweep': one untimed headline sweep, then a plain 1 GiB device-to-device copy
     whose known traffic calibrates the FETCH_SIZE / WRITE_SIZE counters.
     'shares': decode-only launches (28 layers), then prefill-only launches of the
-    last 2048-token chunk (28 layers), Qwen3-0.6B shapes."""
+    last 2048-token chunk (28 layers), Qwen3-0.6B shapes.
+    'shares-8b' / 'shares-32b': 10 decode-only launches, then 10 prefill-only
+    launches of the last chunk of the largest size (two layer pools)."""
     import torch
     from paper_2609_38386_amd import workload as wl
+    if kind in ("shares-8b", "shares-32b"):
+        cfg = wl.CONFIGS["qwen3-8b" if kind == "shares-8b" else "qwen3-32b"]()
+        sw = Sweep(cfg, dev, n_pools=2, layers=2, seed_offset=1, fused=fused)
+        p = max(cfg.chunks)
+        for _ in range(5):
+            sw.iteration(cfg.chunks[0], 0, prefill=False, record=False)
+        for _ in range(5):
+            sw.iteration(p, cfg.prompt_len // p - 1, decoders=False, record=False)
+        torch.cuda.synchronize()
+        print(json.dumps({"decode_launches": 10, "prefill_launches": 10, "p_t": p}), flush=True)
+        return
     cfg = wl.qwen3_0_6b_config()
     sw = Sweep(cfg, dev, n_pools=cfg.layers, layers=cfg.layers, fused=fused)
     if kind == "shares":
