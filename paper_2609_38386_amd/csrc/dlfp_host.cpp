@@ -187,15 +187,21 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
     }
     return n;
   };
-  // Prefill split: long key ranges are cut so that the prefill share offers
-  // about one unit per compute unit (eight resident wavefronts; two prefill
-  // workgroups sharing a CU each run at little more than half speed), never
-  // below 1024 keys.  A launch too small to give every CU a workgroup that
-  // way (decode units counted four to a workgroup, at the split they would
-  // take without prefill) is bound by the latency of its longest unit and of
-  // the merge of its splits: its prefill takes tiles of 32 rows (a merge then
-  // moves a quarter of the bytes) and the shortest split of 256, 512 or 1024
-  // keys that keeps all workgroups within the two a CU holds.
+  // Prefill split.  Prefill alone: the split (multiples of 64 keys, at least
+  // 1024) that minimises an estimate of the launch time, rounds x the time of
+  // the busiest CU, in keys: a unit costs its longest part plus about 300 keys
+  // of prologue, store and merge, and a CU running two units at once runs them
+  // 1.11x faster than one after the other.  The longest part matters: a split
+  // that leaves some tiles whole and cuts others in two makes the launch as
+  // long as the whole ones.  (Fitted to Qwen3-0.6B/8B/32B last chunks, where
+  // it picks the measured best: 0.6B 2048 tokens 143 against 175 us before,
+  // 1024 tokens 83 against 102 us.)  A launch too small to give every CU a
+  // workgroup at 1024-key splits (decode units counted four to a workgroup, at
+  // the split they would take without prefill) is bound by the latency of its
+  // longest unit and of the merge of its splits: its prefill takes tiles of
+  // 32 rows (a merge then moves a quarter of the bytes) and the shortest split
+  // of 256, 512 or 1024 keys that keeps all workgroups within the two a CU
+  // holds.
   int64_t split_p = tn.prefill_split_tokens;
   int64_t dec_wgs0 = 0;
   {
@@ -239,10 +245,33 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
       }
     }
   }
-  if (!split_p)
-    split_p = std::clamp<int64_t>(
-        round_up(std::max<int64_t>(1, ceil_div(pre_keys, std::max<int64_t>(1, resident / 8))), 64),
-        1024, DLFP_MAX_PREFILL_UNIT_KEYS);
+  if (!split_p) {
+    const int64_t cus = std::max<int64_t>(1, resident / 8), slots = 2 * cus;
+    int64_t max_kend = 0;
+    for (int s = 0; s < num_seqs; ++s)
+      if (q_len[s] != 1) max_kend = std::max<int64_t>(max_kend, kv_len[s]);
+    double best = std::numeric_limits<double>::infinity();
+    for (int64_t sp = 1024;; sp += 64) {
+      int64_t n = 0, longest = 0;
+      for (int s = 0; s < num_seqs; ++s) {
+        if (q_len[s] == 1) continue;
+        const int64_t pos0 = kv_len[s] - q_len[s];
+        for (int64_t t0 = 0; t0 < q_len[s]; t0 += tile_tokens) {
+          const int64_t kend = pos0 + t0 + std::min<int64_t>(tile_tokens, q_len[s] - t0);
+          const int64_t part = round_up(ceil_div(kend, ceil_div(kend, sp)), KV_GRANULE_PREFILL);
+          n += hkv * ceil_div(kend, part);
+          longest = std::max(longest, part);
+        }
+      }
+      const double unit = 300.0 + (double)longest;
+      const double e = (double)ceil_div(n, slots) * (n > cus ? 2.0 * (300.0 + longest / 1.11) : unit);
+      if (e < best) {
+        best = e;
+        split_p = sp;
+      }
+      if (sp >= max_kend || sp >= DLFP_MAX_PREFILL_UNIT_KEYS) break;
+    }
+  }
   int64_t split_d = tn.decode_split_tokens;
   if (!split_d) {
     int64_t pre_units = 0;
