@@ -12,9 +12,12 @@ Contents, each written from the definition it cites:
 * ``attention``  -- masked softmax attention over the logical (unpaged)
   sequences of one mixed iteration (Eq. 1's decode and prefill shares,
   Sec. 2.1; chunked prefill over a cached prefix, Sec. 2.1; attention math left
-  unchanged by the controller, Sec. 3.2).  float64.
+  unchanged by the controller, Sec. 3.2): ``attention_rows`` for query rows at
+  given absolute positions, ``attention_sequence`` for a sequence's new
+  tokens.  float64, plain PyTorch CPU ops.
 * ``paging``     -- the gather twin: reads a sequence back out of the paged KV
-  pool through its block table (PagedAttention layout, Sec. 2.1).
+  pool through its block table (PagedAttention layout, Sec. 2.1), token by
+  token (``gather_sequence``) or page by page (``gather_pages``).
 * ``meta``       -- the varlen-metadata twin (cumulative query offsets, query
   positions, slot mapping) and a validity checker for work lists.
 * ``controller`` -- the proportional chunk controller, Eq. 2 (Sec. 3.1), with

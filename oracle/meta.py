@@ -16,6 +16,17 @@ many valid values, so it is not recomputed; ``check_work_list`` verifies the
 properties any valid list must have, and ``check_append_records`` those of the
 records that tell a one-launch append which new tokens to write (each prompt
 token of each KV head exactly once, in runs that stay inside one page).
+
+What the method fixes and what the library's format fixes.  The clause that
+follows from the definition of the iteration (Eq. 1, Sec. 2.1) is coverage:
+every visible (query token, key) pair of every (sequence, KV head) belongs to
+exactly one unit, and the units of one set of rows combine in split order.
+The other clauses check the work-list and workspace format that the library
+declares in its header (``include/dlfp.h``): 128 query rows per prefill unit,
+a 256-byte workspace header, a fixed region of 65536 split counters, partial
+slots of ``rows x 130`` floats padded to 256 bytes, page-aligned key ranges,
+prefill units first and the derived row/position fields.  They guard the
+launch against a malformed list; the paper says nothing about them.
 """
 from __future__ import annotations
 

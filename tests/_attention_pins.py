@@ -1,7 +1,8 @@
 """Pins for the attention oracle, parameterised over the implementation under test.
 
 Each check raises AssertionError when ``impl`` (a function with the signature
-of ``oracle.attention.attention_sequence``) disagrees with something fixed
+of ``oracle.attention.attention_sequence``, or of ``attention_rows`` for the
+rows checks) disagrees with something fixed
 independently of it: brute force in pure-Python float arithmetic, closed forms,
 a library routine, or an invariant of masked softmax attention over a cached
 prefix.  The mutation test runs these same checks against deliberately broken
@@ -145,6 +146,38 @@ def check_decode_equals_last_prefill_row(impl):
     pre = impl(q, k, v, 0.088)
     dec = impl(q[-1:], k, v, 0.088)
     assert np.allclose(dec[0], pre[-1], rtol=0, atol=1e-12)
+
+
+def brute_force_rows(q, k, v, scale, positions):
+    """Pure-Python loops: row r, at absolute position positions[r], sees keys 0..positions[r]."""
+    r_n, hq, d = q.shape
+    _, hkv, _ = k.shape
+    g = hq // hkv
+    out = np.zeros((r_n, hq, d))
+    for r in range(r_n):
+        for h in range(hq):
+            kh = h // g
+            scores = [scale * sum(float(q[r, h, t]) * float(k[j, kh, t]) for t in range(d))
+                      for j in range(int(positions[r]) + 1)]
+            mx = max(scores)
+            ws = [math.exp(x - mx) for x in scores]
+            tot = sum(ws)
+            for t in range(d):
+                out[r, h, t] = sum(w * float(v[j, kh, t]) for j, w in enumerate(ws)) / tot
+    return out
+
+
+def check_rows_brute_force(rows_impl):
+    """Rows at arbitrary positions (out of order, repeated, the first and the last key)."""
+    rng = np.random.default_rng(17)
+    for (n, hq, hkv, d, pos) in [(9, 4, 2, 4, [8, 0, 3, 3, 5]), (6, 2, 1, 16, [5, 1]),
+                                 (12, 8, 2, 8, [11, 7, 0])]:
+        q = _rand(rng, len(pos), hq, d)
+        k = _rand(rng, n, hkv, d)
+        v = _rand(rng, n, hkv, d)
+        got = rows_impl(q, k, v, 0.3, pos)
+        want = brute_force_rows(q, k, v, 0.3, pos)
+        assert np.allclose(got, want, rtol=0, atol=1e-12), (n, hq, hkv, pos)
 
 
 ALL_CHECKS = [check_brute_force, check_large_scores, check_closed_forms, check_library_sdpa,

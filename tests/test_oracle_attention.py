@@ -6,9 +6,9 @@ from oracle import attention as oa
 from oracle import paging
 from paper_2609_38386_amd import workload as wl
 
-from _attention_pins import (check_brute_force, check_chunking_invariance, check_closed_forms,
-                             check_decode_equals_last_prefill_row, check_large_scores,
-                             check_library_sdpa)
+from _attention_pins import (brute_force_attention, check_brute_force, check_chunking_invariance,
+                             check_closed_forms, check_decode_equals_last_prefill_row,
+                             check_large_scores, check_library_sdpa, check_rows_brute_force)
 
 
 def test_brute_force():
@@ -99,17 +99,75 @@ def test_page_permutation_invariance():
     assert np.array_equal(outs[0], outs[1])
 
 
-def test_tiny_iteration_shapes_and_finiteness():
-    seqs = wl.tiny_iteration()
+def test_rows_at_positions_brute_force():
+    check_rows_brute_force(oa.attention_rows)
 
-    class S:
-        def __init__(self, it):
-            self.q_bits = it.stream.q[it.pos0:it.kv_len]
-            self.k_bits = it.stream.k[:it.kv_len]
-            self.v_bits = it.stream.v[:it.kv_len]
-    outs = oa.mixed_iteration([S(it) for it in seqs], 1.0 / np.sqrt(128))
-    assert [o.shape[0] for o in outs] == [128, 1, 1, 1, 1]
-    assert all(np.all(np.isfinite(o)) for o in outs)
+
+def test_rows_of_several_iterations_share_one_key_tensor():
+    """A decoder row at position j over a key tensor that runs past j equals the
+    row over exactly its j + 1 keys: keys beyond a row's position are invisible."""
+    rng = np.random.default_rng(8)
+    k = rng.standard_normal((40, 2, 128))
+    v = rng.standard_normal((40, 2, 128))
+    q = rng.standard_normal((3, 8, 128))
+    got = oa.attention_rows(q, k, v, 0.088, [10, 25, 39])
+    for r, j in enumerate([10, 25, 39]):
+        want = brute_force_attention(q[r:r + 1], k[:j + 1], v[:j + 1], 0.088)
+        assert np.allclose(got[r], want[0], rtol=0, atol=1e-12)
+
+
+def test_rows_reject_positions_outside_the_sequence():
+    z = np.zeros((2, 2, 8))
+    with pytest.raises(ValueError):
+        oa.attention_rows(z, np.zeros((4, 1, 8)), np.zeros((4, 1, 8)), 1.0, [0, 4])
+    with pytest.raises(ValueError):
+        oa.attention_rows(z, np.zeros((4, 1, 8)), np.zeros((4, 1, 8)), 1.0, [-1, 2])
+
+
+def test_bf16_widening_tensor_matches_numpy():
+    bits = np.array([0x3F80, 0xBF80, 0x4049, 0x0000, 0x8000, 0x7F7F, 0x0001, 0x7FC0],
+                    dtype=np.uint16)
+    t = oa.bf16_bits_to_float64_tensor(bits).numpy()
+    n = oa.bf16_bits_to_float64(bits)
+    assert t[2] == 3.140625 and t[6] == float.fromhex("0x1p-133") and np.isnan(t[7])
+    assert np.array_equal(t[:7], n[:7])
+    import torch
+    tt = oa.bf16_bits_to_float64_tensor(torch.from_numpy(bits.view(np.int16))).numpy()
+    assert np.array_equal(tt[:7], n[:7])
+
+
+def test_gather_pages_hand_example():
+    nb, hkv, d = 4, 2, 3
+    kc = np.zeros((nb, hkv, 16, d), dtype=np.uint16)
+    vc = np.zeros((nb, hkv, d, 16), dtype=np.uint16)
+    for b in range(nb):
+        for h in range(hkv):
+            for t in range(16):
+                kc[b, h, t, :] = 1000 * b + 100 * h + t
+                vc[b, h, :, paging.value_position(t)] = 1000 * b + 100 * h + t + 50
+    k, v = paging.gather_pages(kc, vc, np.array([3, 1]), 20)
+    assert k.shape == (20, 2, 3) and v.shape == (20, 2, 3)
+    assert k[0, 0, 0] == 3000 and k[15, 1, 2] == 3115 and k[17, 0, 1] == 1001
+    assert v[17, 1, 0] == 1151 and v[19, 0, 2] == 1053
+    # slot 5 of a value row sits at position 9, slot 9 at 5 (bits 2 and 3 swap)
+    assert v[5, 0, 0] == 3055 and v[9, 0, 0] == 3059
+
+
+@pytest.mark.parametrize("n", [1, 15, 16, 17, 100, 161])
+def test_gather_pages_equals_token_loop(n):
+    import torch
+    rng = np.random.default_rng(n)
+    nb, hkv, d = 24, 3, 8
+    kc = rng.integers(0, 1 << 16, size=(nb, hkv, 16, d), dtype=np.uint16)
+    vc = rng.integers(0, 1 << 16, size=(nb, hkv, d, 16), dtype=np.uint16)
+    row = rng.permutation(nb)[:(n + 15) // 16]
+    k0, v0 = paging.gather_sequence(kc, vc, row, n)
+    k1, v1 = paging.gather_pages(kc, vc, row, n)
+    assert np.array_equal(k0, k1) and np.array_equal(v0, v1)
+    kt, vt = paging.gather_pages(torch.from_numpy(kc.view(np.int16)),
+                                 torch.from_numpy(vc.view(np.int16)), row, n)
+    assert np.array_equal(kt.numpy().view(np.uint16), k0)
+    assert np.array_equal(vt.numpy().view(np.uint16), v0)
 
 
 def test_rejects_bad_shapes():

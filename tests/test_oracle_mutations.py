@@ -11,18 +11,19 @@ import pytest
 
 from oracle import attention as oa
 
-from _attention_pins import ALL_CHECKS
+from _attention_pins import ALL_CHECKS, check_rows_brute_force
 
 MUTANTS = {
     "interleaved GQA heads": ("kh = h // g", "kh = h % hkv"),
     "top-left causal alignment": ("pos0 = n - q_len", "pos0 = 0"),
-    "mask one key short": ("<= positions[:, None]", "< positions[:, None]"),
-    "no causal mask": ("s = np.where(visible, s, -np.inf)", "s = s"),
+    "rows at the wrong positions": ("pos0 + row_idx)", "row_idx)"),
+    "mask one key short": ("<= pos[:, None]", "< pos[:, None]"),
+    "no causal mask": ("s = torch.where(visible, s, -math.inf)", "s = s"),
     "missing softmax scale": ("s = scale * (", "s = ("),
-    "no max subtraction": ("w = np.exp(s - m)", "w = np.exp(s)"),
-    "keys used as values": ("(w @ v[:, kh, :])", "(w @ k[:, kh, :])"),
-    "missing normalisation": ("/ w.sum(axis=1, keepdims=True)", ""),
-    "query head for key head": ("@ k[:, kh, :].T", "@ k[:, h % hkv, :].T"),
+    "no max subtraction": ("w = torch.exp(s - m)", "w = torch.exp(s)"),
+    "keys used as values": ("(w @ v_heads[kh])", "(w @ k_heads[kh])"),
+    "missing normalisation": ("/ w.sum(dim=1, keepdim=True)", ""),
+    "query head for key head": ("@ k_heads[kh].T", "@ k_heads[h % hkv].T"),
 }
 
 
@@ -31,14 +32,19 @@ def _mutant(old, new):
     assert src.count(old) == 1, old
     mod = types.ModuleType("oracle_mutant")
     exec(compile(src.replace(old, new), "oracle_mutant", "exec"), mod.__dict__)
-    return mod.attention_sequence
+    return mod
+
+
+def _checks(mod):
+    return [(c, mod.attention_sequence) for c in ALL_CHECKS] + \
+           [(check_rows_brute_force, mod.attention_rows)]
 
 
 @pytest.mark.parametrize("name", sorted(MUTANTS))
 def test_pins_catch_mutant(name):
-    impl = _mutant(*MUTANTS[name])
+    mod = _mutant(*MUTANTS[name])
     failures = 0
-    for check in ALL_CHECKS:
+    for check, impl in _checks(mod):
         try:
             check(impl)
         except Exception:  # assertion, overflow, shape error: all count as caught
@@ -47,6 +53,6 @@ def test_pins_catch_mutant(name):
 
 
 def test_unmutated_source_passes_every_pin():
-    impl = _mutant("kh = h // g", "kh = h // g")
-    for check in ALL_CHECKS:
+    mod = _mutant("kh = h // g", "kh = h // g")
+    for check, impl in _checks(mod):
         check(impl)
