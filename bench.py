@@ -1,25 +1,28 @@
 #!/usr/bin/env python3
 """Mixed-iteration benchmark of the DLFP hot path on one MI355X.
 
-Headline workload (Qwen3-0.6B attention, per layer x 28 layers): 32 decoders
-with contexts U[512, 2048] beside one 8192-token prompt prefilled in chunks of
-p_t in {64, 128, 256, 512, 1024, 2048}.  One timed step runs the whole sweep:
-for every p_t, the prompt is prefilled in 8192 / p_t mixed iterations while
-each decoder advances one token per iteration.  Each iteration is the full hot
-path -- host metadata build and upload, then for each of the 28 layers (28
-distinct KV pools, so KV reads come from HBM rather than the 256 MB Infinity
-Cache) the KV append and the attention, then the completion-
-timed controller step on the iteration's measured device latency.  The KV
-append and the attention run as one launch (dlfp_append_attention_mixed);
---two-launch times dlfp_kv_append followed by dlfp_attention_mixed instead.
+Headline workload (Qwen3-32B attention shapes on one GPU: 64 query heads, 8
+KV heads, head_dim 128, bf16, 16-token pages, one layer at a time): 256
+decoders with contexts U[2048, 32768] beside one 32768-token prompt
+prefilled in chunks of p_t in {512, 1024, 2048, 4096, 8192}.  One timed step
+runs the whole sweep, 124 chunk iterations: for every p_t the prompt is
+prefilled in 32768 / p_t mixed iterations while each decoder advances one
+token per iteration.  Each iteration is the full hot path -- host metadata
+build and upload, the KV append and the attention (one launch,
+dlfp_append_attention_mixed; --two-launch times dlfp_kv_append followed by
+dlfp_attention_mixed), then the completion-timed controller step on the
+iteration's measured device latency.  The one 18 GB layer pool is far larger
+than the 256 MB Infinity Cache, so every launch reads its keys and values
+from HBM.
 
-Inputs are seeded synthetic N(0,1) bf16 tensors already resident in HBM; the
-decoders' cached history is written straight into the pools.  Attention
-launches are bracketed with HIP events on the stream they run on, which gives
-the per-launch durations behind the roofline figures.  Also reported in the
-same run: latency vs p_t, decode-only and prefill-only shares of the same
-kernel against HBM and bf16 MFMA peaks, the 8B and 32B shapes (first, middle
-and last chunk of each p_t), and the CPU oracle's time on a bounded sample.
+Inputs are seeded synthetic N(0,1) bf16 tensors already resident in HBM.
+Every attention launch of the timed steps is bracketed with HIP events on the
+stream it runs on, which gives the per-launch durations behind the roofline
+figures.  Also reported in the same run: latency vs p_t, decode-only and
+prefill-only shares of the same kernel against the HBM and bf16 MFMA peaks,
+the Qwen3-0.6B sweep (28 layers, 28 pools) and the full Qwen3-8B sweep as
+other shapes, the closed-loop replay, and the CPU oracle's time on a bounded
+sample.
 """
 from __future__ import annotations
 
@@ -41,22 +44,25 @@ METRIC = "mixed-iteration latency vs prefill chunk; decode HBM GB/s %peak; prefi
 def parse_args():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=3)
-    ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--configs", default="qwen3-8b,qwen3-32b",
-                    help="extra shapes measured after the headline (comma list, or 'none')")
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--configs", default="qwen3-0.6b,qwen3-8b",
+                    help="other shapes swept after the headline (comma list, or 'none')")
+    ap.add_argument("--other-steps", type=int, default=3,
+                    help="timed sweeps of each other shape")
+    ap.add_argument("--headline-only", action="store_true",
+                    help="only the headline sweep and its shares (for profiler runs)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--replay-seeds", default="801,802,803",
                     help="seeds of the closed-loop replay (comma list, or 'none')")
     ap.add_argument("--quiet", action="store_true")
     ap.add_argument("--two-launch", action="store_true",
                     help="append with dlfp_kv_append, then dlfp_attention_mixed (instead of "
                          "the one-launch dlfp_append_attention_mixed)")
-    ap.add_argument("--pmc-workload", choices=["sweep", "shares", "shares-8b", "shares-32b"],
-                    default=None,
-                    help="counter-pass workloads: 'sweep' = one headline sweep plus a 1 GiB "
-                         "device copy; 'shares' = decode-only and prefill-only launches")
+    ap.add_argument("--pmc-workload", choices=["sweep-32b", "sweep-0.6b", "shares-8b",
+                                               "shares-32b"], default=None,
+                    help="counter-pass workloads (see pmc_workload)")
     return ap.parse_args()
 
 
@@ -145,7 +151,8 @@ class Sweep:
         max_tok = max(cfg.chunks) + self.n
         self.out = torch.empty((max_tok, self.hq, 128), dtype=torch.bfloat16, device=dev)
         # two staging slots: the next iteration's metadata is built while one runs
-        self.stages = [rt.StagedBatch(self.dims, self.n + 1, max_tok, 65536, dev) for _ in range(2)]
+        self.stages = [rt.StagedBatch(self.dims, self.n + 1, max_tok, 1 << 17, dev)
+                       for _ in range(2)]
         self.stage = self.stages[0]
         self.ws = rt.Workspace(dev, 64 << 20)
         self.timer = D.Timer()
@@ -253,132 +260,174 @@ class Sweep:
         return sorted({0, iters // 2, iters - 1})
 
 
-TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "attention_mixed_qwen3-0.6b_sweep_hbm_traffic.md")
-KERNEL_SOURCES = ("paper_2609_38386_amd/csrc/attention_mixed.hip", "include/dlfp.h",
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "attention_mixed_qwen3-32b_sweep_hbm_traffic.md")
+# Sources whose change can change the HBM traffic of a launch: the kernel, the
+# work-list policy that shapes it, and the headers they share.
+KERNEL_SOURCES = ("paper_2609_38386_amd/csrc/attention_mixed.hip",
+                  "paper_2609_38386_amd/csrc/dlfp_host.cpp", "include/dlfp.h",
                   "paper_2609_38386_amd/csrc/dlfp_internal.h")
 
 
-def profiled_traffic():
-    """HBM bytes per attention launch of the sweep from the committed FETCH_SIZE /
-    WRITE_SIZE summary (calibrated against a device copy), or None when the kernel
-    sources have changed since the counters were taken."""
+def source_hash():
     import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def profiled_traffic():
+    """HBM bytes per attention launch of the headline sweep from the committed
+    FETCH_SIZE / WRITE_SIZE summary (calibrated against a device copy), or None
+    when the kernel or work-list sources have changed since the counters were
+    taken."""
     try:
         text = open(TRAFFIC_PROFILE).read()
-        h = hashlib.sha256()
-        for f in KERNEL_SOURCES:
-            with open(os.path.join(ROOT, f), "rb") as fh:
-                h.update(fh.read())
+        digest = source_hash()
     except OSError:
         return None
     fields = dict(line.split(": ", 1) for line in text.splitlines()
                   if line.startswith(("traffic_bytes_per_launch: ", "source_sha256: ")))
-    if fields.get("source_sha256", "").strip() != h.hexdigest():
+    if fields.get("source_sha256", "").strip() != digest:
         return None
     return int(fields["traffic_bytes_per_launch"])
 
 
-def recorded(cfg, p, c):
-    """Iterations of the timed sweep whose attention launches are bracketed by HIP
-    events: every fourth chunk iteration of each chunk size (chunks 3, 7, 11, ...),
-    a quarter of the sweep in its own mix of chunk sizes."""
+def record_all(cfg, p, c):
+    """Every launch is bracketed by HIP events (a launch lasts milliseconds)."""
+    return True
+
+
+def record_quarter(cfg, p, c):
+    """Every fourth chunk iteration of each chunk size (chunks 3, 7, 11, ...): a
+    quarter of the sweep in its own mix of chunk sizes.  Each event pair adds a
+    dispatch gap of several microseconds, which matters for launches of tens of
+    microseconds."""
     return c % 4 == 3
 
 
-def run_headline(args, dev, log_fn):
+def run_sweep(cfg, dev, log_fn, n_pools, layers, steps, warmup, record, fused=True):
+    """Time `steps` full chunk-size sweeps of `cfg` after `warmup` untimed ones.
+
+    Per iteration: metadata of the next iteration built on the host while the
+    current one runs, `layers` launches (one per layer, rotating over `n_pools`
+    distinct pools), then the controller stepped from the iteration's completion
+    time.  Returns wall time, tokens, per-p_t statistics and the roofline figures
+    of the launches `record` selects."""
     import torch
     from paper_2609_38386_amd import dlfp as D
-    from paper_2609_38386_amd import workload as wl
-    cfg = wl.qwen3_0_6b_config()
     t0 = time.time()
-    sw = Sweep(cfg, dev, n_pools=cfg.layers, layers=cfg.layers, fused=not args.two_launch)
-    log_fn(f"setup {time.time() - t0:.1f}s: {cfg.layers} pools x {sw.num_blocks} blocks")
+    sw = Sweep(cfg, dev, n_pools=n_pools, layers=layers, fused=fused)
+    log_fn(f"{cfg.name}: setup {time.time() - t0:.1f}s: {n_pools} pools x {sw.num_blocks} blocks")
     # decode-only latency of the first iteration sets the controller target (1.2x)
     dec_ms = [sw.iteration(cfg.chunks[0], 0, prefill=False, record=False)[0] for _ in range(3)]
     target = 1.2 * float(np.median(dec_ms))
-    ctrl = D.dlfp_controller_init(target, 2048, 32, 4096, 128)
-
-    iters = [(p, c) for p in cfg.chunks for c in sw.chunks(p, "all")]
+    ctrl = D.dlfp_controller_init(target, 2048, 32, max(4096, max(cfg.chunks)), 128)
+    iters = [(p, c) for p in cfg.chunks for c in range(cfg.prompt_len // p)]
 
     def step(stats):
-        # The next iteration's metadata is built while the current one runs; the
-        # controller is stepped from each iteration's completion time.  HIP events
-        # bracket the attention launches of the sampled iterations only (each event
-        # pair adds a dispatch gap of several microseconds to a layer).
         pr = sw.prepare(*iters[0], slot=0)
         for i, (p, c) in enumerate(iters):
-            rec = recorded(cfg, p, c)
+            rec = record(cfg, p, c)
             sw.launch(pr, record=rec)
             nxt = sw.prepare(*iters[i + 1], slot=(i + 1) & 1) if i + 1 < len(iters) else None
             ms, attn, ql, kl = sw.finish(pr, ctrl)
             pr = nxt
             if stats is None:
                 continue
-            s = stats.setdefault(p, {"iter_ms": [], "attn_ms": 0.0, "bytes": 0, "flops": 0,
-                                     "tokens": 0, "caps": [], "recorded": 0})
+            s = stats.setdefault(p, {"iter_ms": [], "attn_ms": 0.0, "attn_launch_ms": [],
+                                     "bytes": 0, "flops": 0, "tokens": 0, "caps": [],
+                                     "recorded": 0, "by_chunk": {}})
             s["iter_ms"].append(ms)
+            s["by_chunk"].setdefault(c, []).append(ms)
             s["tokens"] += int(ql.sum())
             s["caps"].append(ctrl.cap)
             if rec:
                 s["recorded"] += 1
                 s["attn_ms"] += sum(attn)
+                s["attn_launch_ms"] += list(attn)
                 db, pb, df, pf = attn_work(sw.hq, sw.hkv, ql, kl)
                 ab = append_work(sw.hkv, int(ql.sum())) if sw.fused else 0
-                s["bytes"] += (db + pb + ab) * cfg.layers
-                s["flops"] += (df + pf) * cfg.layers
+                s["bytes"] += (db + pb + ab) * layers
+                s["flops"] += (df + pf) * layers
 
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         step(None)
     torch.cuda.synchronize()
     stats = {}
     t_start = time.perf_counter()
-    for _ in range(args.steps):
+    for _ in range(steps):
         step(stats)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
+    ws_error = D.dlfp_workspace_error(sw.ws.buf)
     tokens = sum(s["tokens"] for s in stats.values())
     attn_ms = sum(s["attn_ms"] for s in stats.values())
-    n_launch = sum(s["recorded"] for s in stats.values()) * cfg.layers
+    n_launch = sum(s["recorded"] for s in stats.values()) * layers
     bytes_all = sum(s["bytes"] for s in stats.values())
     flops_all = sum(s["flops"] for s in stats.values())
     latency = {}
+    lb_all = 0.0
     for p, s in stats.items():
         it = np.asarray(s["iter_ms"])
-        n_l = s["recorded"] * cfg.layers
+        n_l = s["recorded"] * layers
         per_launch_ms = s["attn_ms"] / n_l
         # whole-launch bounds from the algorithmic work of one call: ideal overlap of
         # the HBM and MFMA shares (t_lb) and the two run back to back (t_sum)
         t_b = s["bytes"] / n_l / (HBM_PEAK_GBS * 1e9)
         t_f = s["flops"] / n_l / (MFMA_BF16_PEAK_TFLOPS * 1e12)
+        lb_all += max(t_b, t_f) * n_l
+        chunks = sorted(s["by_chunk"])
+        fml = sorted({chunks[0], chunks[len(chunks) // 2], chunks[-1]})
         latency[str(p)] = {
-            "iter_ms_mean": round(float(it.mean()), 4), "iter_ms_p50": round(float(np.median(it)), 4),
+            "iter_ms_mean": round(float(it.mean()), 4),
+            "iter_ms_p50": round(float(np.median(it)), 4),
             "iter_ms_p90": round(float(np.percentile(it, 90)), 4),
+            "iter_ms_first_mid_last": [round(float(np.median(s["by_chunk"][c])), 4) for c in fml],
             "attn_us_per_layer": round(per_launch_ms * 1e3, 2),
             "attn_GBps": round(s["bytes"] / (s["attn_ms"] * 1e-3) / 1e9, 1),
             "attn_TFLOPs": round(s["flops"] / (s["attn_ms"] * 1e-3) / 1e12, 1),
-            "ttft_proxy_ms": round(float(it.sum()) / args.steps, 3),
-            "iterations": len(it) // args.steps,
-            "iterations_with_launch_events": s["recorded"] // args.steps,
+            "ttft_proxy_ms": round(float(it.sum()) / steps, 3),
+            "iterations": len(it) // steps,
+            "iterations_with_launch_events": s["recorded"] // steps,
             "controller_cap_last": s["caps"][-1],
             "t_lb_us": round(max(t_b, t_f) * 1e6, 2), "t_sum_us": round((t_b + t_f) * 1e6, 2),
             "t_lb_over_measured": round(max(t_b, t_f) / (per_launch_ms * 1e-3), 4),
         }
     avg_launch_s = attn_ms * 1e-3 / n_launch
-    traffic = profiled_traffic()
     ach = (bytes_all / n_launch) / avg_launch_s / 1e9
+    g = sw.hq // sw.hkv
     roofline = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": traffic,
-                "kernel": ("attention_mixed_kernel<2, true> (append + attention)" if sw.fused
-                           else "attention_mixed_kernel<2, false>"),
+                "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None,
+                "kernel": (f"attention_mixed_kernel<{g}, true> (append + attention)" if sw.fused
+                           else f"attention_mixed_kernel<{g}, false>"),
+                "launches_timed": n_launch,
                 "avg_launch_us": round(avg_launch_s * 1e6, 2),
                 "algorithmic_bytes_per_launch": int(bytes_all / n_launch),
-                "algorithmic_tflops": round(flops_all / (attn_ms * 1e-3) / 1e12, 1)}
+                "algorithmic_tflops": round(flops_all / (attn_ms * 1e-3) / 1e12, 1),
+                "t_lb_over_measured": round(lb_all / (attn_ms * 1e-3), 4)}
     shares = measure_shares(sw, cfg)
     result = {"wall": wall, "tokens": tokens, "latency": latency, "roofline": roofline,
-              "shares": shares, "target_ms": target, "decode_only_iter_ms": float(np.median(dec_ms))}
+              "shares": shares, "target_ms": target, "decode_only_iter_ms": float(np.median(dec_ms)),
+              "workspace_error": ws_error, "steps": steps, "warmup": warmup}
     del sw
     torch.cuda.empty_cache()
-    return cfg, result
+    return result
+
+
+def other_shape(name, cfg, r, layers, pools):
+    """Summary of a sweep measured beside the headline."""
+    return {"shape": f"Hq{cfg.shape.num_q_heads}/Hkv{cfg.shape.num_kv_heads}/d128",
+            "decoders": cfg.n_decoders, "ctx": [cfg.ctx_lo, cfg.ctx_hi],
+            "prompt_len": cfg.prompt_len, "chunks": list(cfg.chunks),
+            "model_layers": cfg.layers, "layers_per_iteration_timed": layers,
+            "distinct_layer_pools": pools, "steps": r["steps"],
+            "tokens_per_s": round(r["tokens"] / r["wall"], 1),
+            "ms_per_sweep": round(r["wall"] * 1e3 / r["steps"], 3),
+            "roofline": r["roofline"], "latency_vs_pt": r["latency"], "shares": r["shares"],
+            "decode_only_iter_ms": round(r["decode_only_iter_ms"], 4),
+            "workspace_error": r["workspace_error"]}
 
 
 def measure_shares(sw, cfg, min_launches=20):
@@ -431,45 +480,6 @@ def measure_shares(sw, cfg, min_launches=20):
                        "launches": len(t)}
     out["prefill_last_chunk"] = pre
     return out
-
-
-def run_extra(name, dev, log_fn, fused=True):
-    """First, middle and last chunk of every p_t for a larger shape."""
-    import torch
-    from paper_2609_38386_amd import dlfp as D
-    from paper_2609_38386_amd import workload as wl
-    cfg = wl.CONFIGS[name]()
-    t0 = time.time()
-    layers_timed = 2 if cfg.layers > 1 else 1   # each pool far exceeds the 256 MB cache
-    sw = Sweep(cfg, dev, n_pools=layers_timed, layers=layers_timed, seed_offset=1, fused=fused)
-    log_fn(f"{name}: setup {time.time() - t0:.1f}s, {sw.num_blocks} blocks/pool")
-    dec_ms = [sw.iteration(cfg.chunks[0], 0, prefill=False)[0] for _ in range(2)]
-    ctrl = D.dlfp_controller_init(1.2 * float(np.median(dec_ms)), 2048, 32, 8192, 128)
-    lat = {}
-    for p in cfg.chunks:
-        ms_l, attn_l, b_l, f_l = [], 0.0, 0, 0
-        for c in sw.chunks(p, "fml"):
-            sw.iteration(p, c, ctrl=ctrl)          # untimed pass warms the work list path
-            ms, a, ql, kl = sw.iteration(p, c, ctrl=ctrl)
-            ms_l.append(ms / layers_timed)
-            attn_l += sum(a)
-            db, pb, df, pf = attn_work(sw.hq, sw.hkv, ql, kl)
-            ab = append_work(sw.hkv, int(ql.sum())) if fused else 0
-            b_l += (db + pb + ab) * layers_timed
-            f_l += (df + pf) * layers_timed
-        sec = attn_l * 1e-3
-        lat[str(p)] = {"iter_ms_per_layer_first_mid_last": [round(x, 4) for x in ms_l],
-                       "model_iter_ms_mean": round(float(np.mean(ms_l)) * cfg.layers, 3),
-                       "attn_GBps": round(b_l / sec / 1e9, 1),
-                       "attn_TFLOPs": round(f_l / sec / 1e12, 1)}
-    shares = measure_shares(sw, cfg)
-    del sw
-    torch.cuda.empty_cache()
-    return {"shape": f"Hq{cfg.shape.num_q_heads}/Hkv{cfg.shape.num_kv_heads}/d128",
-            "decoders": cfg.n_decoders, "ctx": [cfg.ctx_lo, cfg.ctx_hi],
-            "prompt_len": cfg.prompt_len, "layers": cfg.layers,
-            "decode_only_ms_per_layer": round(float(np.median(dec_ms)) / layers_timed, 4),
-            "latency_vs_pt": lat, "shares": shares}
 
 
 # ----------------------------------------------------------------------------- replay
@@ -557,41 +567,58 @@ def run_overlap_replay(dev, seed, rate, log_fn):
 
 # ----------------------------------------------------------------------------- CPU baseline
 
-def cpu_baseline(seconds):
-    """The float64 oracle on a bounded sample: one layer of one Qwen3-0.6B mixed
-    iteration (p_t = 512 at chunk 7, plus the 32 decoders), repeated."""
-    from threadpoolctl import threadpool_info
+def cpu_baseline(dev, seconds, p=512, c=32):
+    """The float64 oracle on a bounded sample of the headline workload: iteration
+    (p_t, chunk c) of the Qwen3-32B sweep -- the prompt chunk, then decoders one at
+    a time until `seconds` have passed -- from the paged bf16 pool to the outputs
+    (the oracle's page gather, exact widening to float64, masked softmax
+    attention).  The pool pages of the sampled sequences are drawn on the device
+    and copied to the host before the clock starts.  The per-iteration time is the
+    prompt's plus the mean decoder's times the 256 decoders."""
+    import torch
     from oracle import attention as oa
+    from oracle import paging as op
+    from paper_2609_38386_amd import runtime as rt
     from paper_2609_38386_amd import workload as wl
-    cfg = wl.qwen3_0_6b_config()
-    p, c = 512, 7
-    dec = cfg.decoder_streams()
+    cfg = wl.qwen3_32b_config()
+    hq, hkv = cfg.shape.num_q_heads, cfg.shape.num_kv_heads
     ctx = cfg.decoder_contexts()
-    prompt = cfg.prompt_stream()
-    seqs = [(prompt, p, (c + 1) * p)] + [(dec[i], 1, int(ctx[i]) + c) for i in range(cfg.n_decoders)]
-    data = [(oa.bf16_bits_to_float64(s.q[n - q:n]), oa.bf16_bits_to_float64(s.k[:n]),
-             oa.bf16_bits_to_float64(s.v[:n])) for s, q, n in seqs]
+    its = cfg.iteration(p, c)                  # prompt first, then the decoders
+    n_sample = min(len(its), 65)               # prompt + up to 64 decoders staged
+    pages = [wl.pages_for(kl) for _, _, kl in its[:n_sample]]
+    nb = int(sum(pages))
+    bt = wl.block_tables(cfg.seed, pages, nb)
+    pool = rt.KVPool(nb, hkv, dev)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(cfg.seed + 7)
+    pool.k.normal_(generator=gen)
+    pool.v.normal_(generator=gen)
+    q = torch.empty((p + n_sample - 1, hq, 128), dtype=torch.bfloat16, device=dev)
+    q.normal_(generator=gen)
+    k_host, v_host = pool.k.view(torch.int16).cpu(), pool.v.view(torch.int16).cpu()
+    q_host = q.view(torch.int16).cpu()
+    del pool, q
+    torch.cuda.empty_cache()
     scale = 1.0 / math.sqrt(128)
-    reps, t0 = 0, time.perf_counter()
-    t_pre = t_dec = 0.0
-    while True:
-        for i, (qq, kk, vv) in enumerate(data):
-            ts = time.perf_counter()
-            oa.attention_sequence(qq, kk, vv, scale)
-            if i == 0:
-                t_pre += time.perf_counter() - ts
-            else:
-                t_dec += time.perf_counter() - ts
-        reps += 1
-        el = time.perf_counter() - t0
-        if el >= seconds:
-            break
-    per_layer = el / reps
+
+    def one(i):
+        _, ql, kl = its[i]
+        k, v = op.gather_pages(k_host, v_host, bt[i], kl)
+        r0 = 0 if i == 0 else p + i - 1
+        qq = oa.bf16_bits_to_float64_tensor(q_host[r0:r0 + ql])
+        oa.attention_rows(qq, oa.bf16_bits_to_float64_tensor(k),
+                          oa.bf16_bits_to_float64_tensor(v), scale, np.arange(kl - ql, kl))
+
+    t0 = time.perf_counter()
+    one(0)
+    t_prompt = time.perf_counter() - t0
+    n_dec, t1 = 0, time.perf_counter()
+    while n_dec < n_sample - 1 and (n_dec < 2 or time.perf_counter() - t0 < seconds):
+        one(1 + n_dec)
+        n_dec += 1
+    t_dec = (time.perf_counter() - t1) / n_dec
+    per_iter = t_prompt + t_dec * cfg.n_decoders
     tokens = p + cfg.n_decoders
-    info = threadpool_info()
-    threads = max([d.get("num_threads", 1) for d in info] or [1])
-    blas = ", ".join(sorted({f"{d.get('internal_api')} {d.get('version')}" for d in info
-                             if d.get("user_api") == "blas"})) or "none loaded"
     model = "unknown"
     try:
         with open("/proc/cpuinfo") as f:
@@ -601,24 +628,26 @@ def cpu_baseline(seconds):
                     break
     except OSError:
         pass
-    return {"value": round(tokens / (per_layer * cfg.layers), 2), "unit": "tok/s",
-            "cores": int(threads), "kind": "oracle",
-            "sample": (f"float64 oracle, {reps} repetitions of one layer of one Qwen3-0.6B mixed "
-                       f"iteration (p_t={p} at chunk {c}, 32 decoders), "
-                       f"{per_layer * 1e3:.1f} ms per layer, scaled to 28 layers"),
-            "seconds": round(el, 2),
-            "prefill_ms_per_layer": round(t_pre * 1e3 / reps, 2),
-            "decode_ms_per_layer": round(t_dec * 1e3 / reps, 2),
-            "cpu_model": model, "nproc": os.cpu_count(), "blas": blas}
+    return {"value": round(tokens / per_iter, 2), "unit": "tok/s",
+            "cores": int(torch.get_num_threads()), "kind": "oracle",
+            "sample": (f"float64 oracle (PyTorch CPU ops) on iteration p_t={p}, chunk {c} of the "
+                       f"Qwen3-32B sweep: the {p}-token prompt chunk over a {c * p}-token prefix "
+                       f"({t_prompt:.2f} s) and {n_dec} of the 256 decoders ({t_dec * 1e3:.0f} ms "
+                       f"each), scaled to the whole iteration ({per_iter:.1f} s for {tokens} "
+                       f"tokens)"),
+            "seconds": round(time.perf_counter() - t0, 2),
+            "prefill_s_per_iteration": round(t_prompt, 3),
+            "decode_s_per_iteration": round(t_dec * cfg.n_decoders, 3),
+            "cpu_model": model, "nproc": os.cpu_count()}
 
 
 # ----------------------------------------------------------------------------- main
 
 def pmc_workload(dev, kind, fused=True):
-    """'sweep': one untimed headline sweep, then a plain 1 GiB device-to-device copy
-    whose known traffic calibrates the FETCH_SIZE / WRITE_SIZE counters.
-    'shares': decode-only launches (28 layers), then prefill-only launches of the
-    last 2048-token chunk (28 layers), Qwen3-0.6B shapes.
+    """Workloads for counter passes (no timing).
+    'sweep-32b' / 'sweep-0.6b': one untimed sweep of the shape (the headline's launches;
+    0.6B over its 28 pools), then a plain 1 GiB device-to-device copy whose known
+    traffic calibrates the FETCH_SIZE / WRITE_SIZE counters.
     'shares-8b' / 'shares-32b': 10 decode-only launches, then 10 prefill-only
     launches of the last chunk of the largest size (two layer pools)."""
     import torch
@@ -634,13 +663,8 @@ def pmc_workload(dev, kind, fused=True):
         torch.cuda.synchronize()
         print(json.dumps({"decode_launches": 10, "prefill_launches": 10, "p_t": p}), flush=True)
         return
-    cfg = wl.qwen3_0_6b_config()
+    cfg = wl.qwen3_32b_config() if kind == "sweep-32b" else wl.qwen3_0_6b_config()
     sw = Sweep(cfg, dev, n_pools=cfg.layers, layers=cfg.layers, fused=fused)
-    if kind == "shares":
-        sw.iteration(cfg.chunks[0], 0, prefill=False, record=False)
-        sw.iteration(2048, cfg.prompt_len // 2048 - 1, decoders=False, record=False)
-        print(json.dumps({"decode_launches": cfg.layers, "prefill_launches": cfg.layers}))
-        return
     n = 0
     for p in cfg.chunks:
         for c in sw.chunks(p, "all"):
@@ -666,6 +690,7 @@ def main():
         sys.exit(2)
     import torch
     from paper_2609_38386_amd import dlfp as D
+    from paper_2609_38386_amd import workload as wl
     D.lib()  # fail loudly without the HIP library
     if not torch.cuda.is_available():
         print("bench.py needs a HIP device", file=sys.stderr)
@@ -675,21 +700,42 @@ def main():
         pmc_workload(dev, args.pmc_workload, fused=not args.two_launch)
         return
     logf = lambda *a: log(args, *a)  # noqa: E731
-    cfg, r = run_headline(args, dev, logf)
+    fused = not args.two_launch
+    cfg = wl.qwen3_32b_config()
+    r = run_sweep(cfg, dev, logf, n_pools=1, layers=1, steps=args.steps, warmup=args.warmup,
+                  record=record_all, fused=fused)
     logf(f"headline done: {r['wall']:.2f}s for {args.steps} steps")
+    errors = {"qwen3-32b": r["workspace_error"]}
+    if fused:
+        r["roofline"]["traffic"] = profiled_traffic()
+    cpu = None
+    if not args.no_cpu_baseline and not args.headline_only:
+        cpu = cpu_baseline(dev, args.cpu_seconds)
+        logf(f"cpu baseline done: {cpu['value']} tok/s")
     extras = {}
-    names = [] if args.configs in ("", "none") else args.configs.split(",")
+    names = [] if args.configs in ("", "none") or args.headline_only else args.configs.split(",")
     for name in names:
-        extras[name] = run_extra(name.strip(), dev, logf, fused=not args.two_launch)
-        logf(f"{name} done")
+        name = name.strip()
+        ocfg = wl.CONFIGS[name]()
+        if name == "qwen3-0.6b":   # 28 distinct pools: one pool (154 MB) fits the 256 MB cache
+            pools, layers, steps, rec = ocfg.layers, ocfg.layers, args.other_steps, record_quarter
+        else:                      # each pool is far larger than the cache
+            pools, layers, steps, rec = 2, 2, args.other_steps, record_all
+        o = run_sweep(ocfg, dev, logf, n_pools=pools, layers=layers, steps=steps, warmup=1,
+                      record=rec, fused=fused)
+        extras[name] = other_shape(name, ocfg, o, layers, pools)
+        errors[name] = o["workspace_error"]
+        logf(f"{name} done: {o['tokens'] / o['wall']:.0f} tok/s")
     replay = None
-    if args.replay_seeds not in ("", "none"):
+    if args.replay_seeds not in ("", "none") and not args.headline_only:
         seeds = [int(x) for x in args.replay_seeds.split(",")]
         replay = run_replays(dev, seeds, logf)
         replay["overlap_20_req_s"] = run_overlap_replay(dev, seeds[0], 20.0, logf)
-    cpu = None
-    if not args.no_cpu_baseline:
-        cpu = cpu_baseline(args.cpu_seconds)
+    if any(errors.values()):
+        print(f"bench.py: the workspace error word is set after the timed launches: {errors} "
+              "(1 = a block id outside the pool, 2 = a wait for the append records ran out); "
+              "no result is reported", file=sys.stderr)
+        sys.exit(1)
     ms_per_step = r["wall"] * 1e3 / args.steps
     value = r["tokens"] / r["wall"]
     line = {
@@ -697,11 +743,12 @@ def main():
         "unit": "tok/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 3), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": ("qwen3-0.6b attention x28 layers: 32 decoders ctx U[512,2048] + "
-                                "8192-token prompt chunked at p_t in {64..2048}, full sweep per step"),
-                   "num_q_heads": 16, "num_kv_heads": 8, "head_dim": 128, "page": 16,
-                   "decoders": 32, "prompt_len": 8192, "chunks": list(cfg.chunks),
-                   "layers": 28, "distinct_layer_pools": 28,
+        "config": {"workload": ("qwen3-32b attention, one layer, all 64 query heads on one GPU: "
+                                "256 decoders ctx U[2048,32768] + 32768-token prompt chunked at "
+                                "p_t in {512..8192}, full sweep (124 chunk iterations) per step"),
+                   "num_q_heads": 64, "num_kv_heads": 8, "head_dim": 128, "page": 16,
+                   "decoders": cfg.n_decoders, "prompt_len": cfg.prompt_len,
+                   "chunks": list(cfg.chunks), "layers": 1, "distinct_layer_pools": 1,
                    "tokens_per_step": r["tokens"] // args.steps},
         "roofline": r["roofline"],
         "cpu_baseline": cpu,
@@ -709,7 +756,8 @@ def main():
         "shares": r["shares"],
         "controller": {"target_ms": round(r["target_ms"], 4),
                        "decode_only_iter_ms": round(r["decode_only_iter_ms"], 4),
-                       "rule": "Eq. 2, completion-timed (HIP events), caps 32..4096, quantum 128"},
+                       "rule": "Eq. 2, completion-timed (HIP events), quantum 128"},
+        "workspace_error": errors,
         "other_shapes": extras,
         "replay": replay,
         "paper_context": "27.7% mean P99 ITL reduction, Qwen3-0.6B BF16, 1x A100 80GB (context only)",

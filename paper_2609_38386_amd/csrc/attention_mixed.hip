@@ -822,6 +822,89 @@ __device__ void prefill_unit(const Args& a, const int32_t* it, char* smem, int* 
     __hip_atomic_store(group_counter(a.ws, grp), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// Last arriver of a decode split group: merges the group's partial results
+// (O[G][128], m[G], l[G] per split, in split order) into the output.  Lane
+// `lane` writes dims 2 lane and 2 lane + 1 of every head; obase is the
+// element offset of those dims of the group's first head.
+template <int G>
+__device__ __forceinline__ void decode_merge(const Args& a, const Slots sl, int slot_floats,
+                                             int nsplits, int64_t obase, int grp) {
+  const int lane = threadIdx.x & 63;
+  // Entry f = j G + h stands for head h of split j.  Per batch
+  // of up to 64 entries, lane e loads entry e's maximum and row sum while
+  // every lane loads its two dims of the batch's entries (in groups of 16,
+  // only as many groups as the batch has entries), so a batch costs one
+  // memory round trip; the running per-head maximum rescales what earlier
+  // batches summed, and entries are accumulated in split order.
+  const int nf = nsplits * G;
+  float M[G], lsum[G], acc0[G], acc1[G];
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    M[h] = NEG_BIG;
+    lsum[h] = acc0[h] = acc1[h] = 0.f;
+  }
+  for (int f0 = 0; f0 < nf; f0 += 64) {
+    const int n = min(64, nf - f0);
+    const int fl = f0 + min(lane, n - 1);
+    const int lbase = (fl / G) * slot_floats + G * D + fl % G;
+    const float mf = lane < n ? pload1(sl, lbase) : NEG_BIG;
+    const float lf = pload1(sl, lbase + G);
+    f32x2_t v[4][16];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if (16 * q < n) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int fe = f0 + min(16 * q + e, n - 1);
+          v[q][e] = pload2(sl, (fe / G) * slot_floats + (fe % G) * D + 2 * lane);
+        }
+      }
+    }
+    // Batch maximum of head lane % G (f0 is a multiple of 64, so entry
+    // f0 + e belongs to head e % G).
+    float bm = mf;
+#pragma unroll
+    for (int sh = G; sh < 64; sh <<= 1) bm = fmaxf(bm, shfl_xor(bm, sh));
+    float mh = NEG_BIG;
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      const float mnew = fmaxf(M[h], __builtin_bit_cast(float, __builtin_amdgcn_readlane(
+                                                                  __builtin_bit_cast(int, bm), h)));
+      const float rs = fexp2(M[h] - mnew);
+      M[h] = mnew;
+      lsum[h] *= rs;
+      acc0[h] *= rs;
+      acc1[h] *= rs;
+      if (lane % G == h) mh = mnew;
+    }
+    const float wf = lane < n ? fexp2(mf - mh) : 0.f;
+    const float wl = wf * lf;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if (16 * q < n) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int src = 16 * q + e;  // weights of entries past the batch are zero
+          const float w = __builtin_bit_cast(float, __builtin_amdgcn_readlane(
+                                                        __builtin_bit_cast(int, wf), src));
+          const float lw = __builtin_bit_cast(float, __builtin_amdgcn_readlane(
+                                                         __builtin_bit_cast(int, wl), src));
+          lsum[e % G] += lw;
+          acc0[e % G] += w * v[q][e][0];
+          acc1[e % G] += w * v[q][e][1];
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    const float inv = 1.f / lsum[h];
+    store2(a, obase + h * D, acc0[h] * inv, acc1[h] * inv);
+  }
+  if (lane == 0)
+    __hip_atomic_store(group_counter(a.ws, grp), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // ---------------------------------------------------------------- decode
 
 // Wave-private LDS slice: two page slots, each a K page (token rows, 16-byte
@@ -1134,79 +1217,265 @@ __device__ int decode_unit(const Args& a, const int32_t* it_g, char* wl, bool ta
   old = __shfl(old, 0);
   if (old != nsplits - 1) return ticket_v;
 
-  // Last arriver.  Entry f = j G + h stands for head h of split j.  Per batch
-  // of up to 64 entries, lane e loads entry e's maximum and row sum while
-  // every lane loads its two dims of the batch's entries (in groups of 16,
-  // only as many groups as the batch has entries), so a batch costs one
-  // memory round trip; the running per-head maximum rescales what earlier
-  // batches summed, and entries are accumulated in split order.
-  const int nf = nsplits * G;
-  float M[G], lsum[G], acc0[G], acc1[G];
+  decode_merge<G>(a, sl, slot_floats, nsplits, obase, grp);
+  return ticket_v;
+}
+
+// ---------------------------------------------------------------- decode on the matrix cores
+
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+
+// Decode unit for g >= 4 query heads per KV head.  The unit's g heads are the
+// columns of 16x16 matrix products (padded to 16 with zero queries): per page,
+// the scores are S^T = K Q^T (four v_mfma_f32_16x16x32_bf16 over the 128
+// dims) and the output advances by O^T += V^T P^T (eight
+// v_mfma_f32_16x16x16_bf16 over the page's 16 keys), so the VALU only forms
+// the softmax.  Lane l owns head column l % 16 and accumulator rows
+// 4 (l / 16) .. + 3.  Row r of the K operand (and so of S^T) is token slot
+// vt_pos(r) of the page: a lane's four rows are then four consecutive
+// positions of a value-page row (the cache keeps V^T pages with slot t at
+// position vt_pos(t)), so the probabilities go from the score accumulator
+// straight into the B operand of the PV product, and a lane's V^T operand is
+// one 8-byte LDS read.  Per-head maxima combine the four lane groups with
+// permlane swaps; the reference maximum is raised lazily, as in the prefill
+// tiles.
+//
+// LDS page slots (two per wavefront, as for decode_unit): K page row R keeps
+// its 16-byte chunk x at position x ^ R; V^T row d (32 bytes) keeps its two
+// 16-byte halves swapped when bit 3 of d is set.  Either way the lanes that
+// LDS serves together read distinct banks.  The page pipeline, the prologue,
+// the queue tickets, the one-launch append and the split merge are those of
+// decode_unit.
+template <int G, bool APP>
+__device__ int decode_unit_mfma(const Args& a, const int32_t* it_g, char* wl, bool take_ticket) {
+  static_assert(G >= 4 && G <= 16, "heads must fit the 16 columns");
+  const int lane = threadIdx.x & 63;
+  const int col = lane & 15, gq = lane >> 4;
+  const record_ptr it = as_record(it_g);
+  const int s = it[DLFP_W_SEQ], kh = it[DLFP_W_KVHEAD];
+  const int kb = it[DLFP_W_KVBEGIN], ke = it[DLFP_W_KVEND];
+  const int nsplits = it[DLFP_W_NSPLITS];
+  const int tok = it[DLFP_W_QROW0];
+  const int newpos = it[DLFP_W_QPOS0];
+  const int first_blk = it[DLFP_W_PAGE0], second_blk = it[DLFP_W_PAGE1];
+  const int grp = it[DLFP_W_GROUP], wsgroup = it[DLFP_W_WSGROUP], split = it[DLFP_W_SPLIT];
+  const int32_t* bt = a.block_table + (int64_t)s * a.max_blocks;
+  int32_t* ptab = reinterpret_cast<int32_t*>(wl + 2 * DEC_PAGE_SLOT + 16 * 16 * 2);
+
+  const bool deep = a.num_prefill == 0;
+  const int p_begin = kb / PAGE, p_end = (ke + PAGE - 1) / PAGE;
+  const int npages = p_end - p_begin;
+  uint32_t kofs[4], vofs[4];
 #pragma unroll
-  for (int h = 0; h < G; ++h) {
-    M[h] = NEG_BIG;
-    lsum[h] = acc0[h] = acc1[h] = 0.f;
+  for (int j = 0; j < 4; ++j) {
+    const int ck = 64 * j + lane;  // LDS chunk this lane fills
+    const int R = ck >> 4, xs = ck & 15;
+    kofs[j] = R * 256 + ((xs ^ R) << 4);
+    const int d = ck >> 1, hs = ck & 1;
+    vofs[j] = d * 32 + ((hs ^ ((d >> 3) & 1)) << 4);
   }
-  for (int f0 = 0; f0 < nf; f0 += 64) {
-    const int n = min(64, nf - f0);
-    const int fl = f0 + min(lane, n - 1);
-    const int lbase = (fl / G) * slot_floats + G * D + fl % G;
-    const float mf = lane < n ? pload1(sl, lbase) : NEG_BIG;
-    const float lf = pload1(sl, lbase + G);
-    f32x2_t v[4][16];
+  const uint32_t lds_wave = (uint32_t)uniform((int)lds_addr(wl));
+  auto issue_block = [&](int raw, int slot) {
+    const bool ok = (unsigned)raw < (unsigned)a.num_blocks;
+    if (!ok && lane == 0) raise_error(a.ws);
+    const int64_t base = ((int64_t)(ok ? raw : 0) * a.hkv + kh) * PAGE_ELEMS;
+    const char* ksrc = reinterpret_cast<const char*>(a.kc + base);
+    const char* vsrc = reinterpret_cast<const char*>(a.vc + base);
+    const uint32_t dst = lds_wave + uniform(slot) * DEC_PAGE_SLOT;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      if (16 * q < n) {
+    for (int j = 0; j < 4; ++j) {
+      lds_copy16(ksrc + kofs[j], dst + j * 1024);
+      lds_copy16(vsrc + vofs[j], dst + PAGE_ELEMS * 2 + j * 1024);
+    }
+  };
+  auto issue = [&](int p, int slot) { issue_block(uniform(ptab[p - p_begin]), slot); };
+  auto wait_page = [&](bool next_in_flight) {
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    if (next_in_flight)
+      __builtin_amdgcn_s_waitcnt(0x0F78);  // vmcnt(8)
+    else
+      __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  };
+
+  // Prologue (one round trip after the work record): the first page, the
+  // queries as the B operand (lane holds dims 32 kk + 8 (l / 16) .. + 8 of head
+  // column l % 16, zero past the unit's g heads), the unit's block ids and
+  // (append launches) the new token's key row and value pair.
+  issue_block(first_blk, 0);
+  bf16x8_t qb[4];
+  {
+    const uint16_t* qp = a.q + ((int64_t)tok * a.hq + kh * G + min(col, G - 1)) * D + 8 * gq;
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int fe = f0 + min(16 * q + e, n - 1);
-          v[q][e] = pload2(sl, (fe / G) * slot_floats + (fe % G) * D + 2 * lane);
-        }
+    for (int kk = 0; kk < 4; ++kk) {
+      const u32x4_t v = *reinterpret_cast<const u32x4_t*>(qp + 32 * kk);
+      qb[kk] = __builtin_bit_cast(bf16x8_t, col < G ? v : u32x4_t{0u, 0u, 0u, 0u});
+    }
+  }
+  constexpr int PTV = DEC_PTAB / 64;
+  int ptv[PTV];
+#pragma unroll
+  for (int k = 0; k < PTV; ++k) {
+    const int i = lane + 64 * k;
+    ptv[k] = i < npages ? bt[p_begin + i] : 0;
+  }
+  const bool own_new = APP && newpos < ke;
+  const int new_page = newpos / PAGE, new_off = newpos % PAGE;
+  u32x4_t kn = {0u, 0u, 0u, 0u};
+  uint32_t vn = 0u;
+  if (own_new) {
+    const int64_t src = ((int64_t)tok * a.hkv + kh) * D;
+    if (lane < 16) kn = *reinterpret_cast<const u32x4_t*>(a.k_new + src + 8 * lane);
+    vn = *reinterpret_cast<const uint32_t*>(a.v_new + src + 2 * lane);
+  }
+  if (deep && npages > 1) issue_block(second_blk, 1);
+  wait_memory_complete();
+#pragma unroll
+  for (int k = 0; k < PTV; ++k)
+    if (lane + 64 * k < npages) ptab[lane + 64 * k] = ptv[k];
+  wave_sync();
+  if (own_new) {
+    const int raw = ptab[new_page - p_begin];
+    if ((unsigned)raw < (unsigned)a.num_blocks) {
+      const int64_t base = ((int64_t)raw * a.hkv + kh) * PAGE_ELEMS;
+      uint16_t* kc = const_cast<uint16_t*>(a.kc);
+      uint16_t* vc = const_cast<uint16_t*>(a.vc);
+      if (lane < 16) *reinterpret_cast<u32x4_t*>(kc + base + new_off * D + 8 * lane) = kn;
+      vc[base + (2 * lane) * PAGE + vt_pos(new_off)] = (uint16_t)(vn & 0xFFFFu);
+      vc[base + (2 * lane + 1) * PAGE + vt_pos(new_off)] = (uint16_t)(vn >> 16);
+    }
+  }
+
+  float m_run = NEG_BIG, l_run = 0.f;
+  f32x4_t o[8];
+#pragma unroll
+  for (int mb = 0; mb < 8; ++mb) o[mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  const float c = a.scale_log2;
+  int ticket_v = 0;
+  const int ticket_page = max(p_begin, p_end - 4);
+  // This lane's K operand row (token slot vt_pos(col)), the token slot of its
+  // first accumulator row (vt_pos(4 gq)), and its V^T operand's byte offset
+  // inside a 16-row block (row col, positions 4 gq .. + 3).
+  const int ra = vt_pos(col);
+  const int slot0 = vt_pos(4 * gq);
+  const int vbyte = col * 32 + (((gq >> 1) ^ ((col >> 3) & 1)) << 4) + 8 * (gq & 1);
+
+  auto process = [&](int p, int slot) {
+    char* kl = wl + slot * DEC_PAGE_SLOT;
+    char* vl = kl + PAGE_ELEMS * 2;
+    wait_page(deep && p + 1 < p_end);
+    wave_sync();
+    if (!deep && p + 1 < p_end) issue(p + 1, slot ^ 1);  // that slot was consumed
+    if (take_ticket && p == ticket_page && lane == 0)
+      ticket_v = __hip_atomic_fetch_add(header_word(a.ws, HDR_TICKET), 1, __ATOMIC_RELAXED,
+                                        __HIP_MEMORY_SCOPE_AGENT);
+    if (p * PAGE + PAGE > ke) {
+      // Values past the unit's last key are zeroed (a probability of 0 times
+      // a NaN left in an unused slot would still be NaN).
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int ck = 64 * j + lane;
+        const int d = ck >> 1, h = (ck & 1) ^ ((d >> 3) & 1);
+        u32x4_t* v = reinterpret_cast<u32x4_t*>(vl + ck * 16);
+        *v = mask_elems(*v, ke, [&](int e) { return p * PAGE + vt_pos(8 * h + e); });
       }
     }
-    // Batch maximum of head lane % G (f0 is a multiple of 64, so entry
-    // f0 + e belongs to head e % G).
-    float bm = mf;
-#pragma unroll
-    for (int sh = G; sh < 64; sh <<= 1) bm = fmaxf(bm, shfl_xor(bm, sh));
-    float mh = NEG_BIG;
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      const float mnew = fmaxf(M[h], __builtin_bit_cast(float, __builtin_amdgcn_readlane(
-                                                                  __builtin_bit_cast(int, bm), h)));
-      const float rs = fexp2(M[h] - mnew);
-      M[h] = mnew;
-      lsum[h] *= rs;
-      acc0[h] *= rs;
-      acc1[h] *= rs;
-      if (lane % G == h) mh = mnew;
+    if (own_new && p == new_page) {
+      if (lane < 16)
+        *reinterpret_cast<u32x4_t*>(kl + new_off * 256 + ((lane ^ new_off) << 4)) = kn;
+      const int sp = vt_pos(new_off), half = sp >> 3;
+      const int d0 = 2 * lane, d1 = 2 * lane + 1;
+      *reinterpret_cast<uint16_t*>(vl + d0 * 32 + ((half ^ ((d0 >> 3) & 1)) << 4) + 2 * (sp & 7)) =
+          (uint16_t)(vn & 0xFFFFu);
+      *reinterpret_cast<uint16_t*>(vl + d1 * 32 + ((half ^ ((d1 >> 3) & 1)) << 4) + 2 * (sp & 7)) =
+          (uint16_t)(vn >> 16);
     }
-    const float wf = lane < n ? fexp2(mf - mh) : 0.f;
-    const float wl = wf * lf;
+    wave_sync();  // fixed-up page visible to every lane
+
+    // S^T = K Q^T: rows = token slots vt_pos(r), columns = heads.
+    f32x4_t sacc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      if (16 * q < n) {
+    for (int kk = 0; kk < 4; ++kk) {
+      const bf16x8_t kf =
+          *reinterpret_cast<const bf16x8_t*>(kl + ra * 256 + (((4 * kk + gq) ^ ra) << 4));
+      sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qb[kk], sacc, 0, 0, 0);
+    }
+    // Rows 4 gq + i hold slots slot0 + i; keys at or past ke are masked.
+    float sc[4];
+    float mx = -__builtin_inff();
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int src = 16 * q + e;  // weights of entries past the batch are zero
-          const float w = __builtin_bit_cast(float, __builtin_amdgcn_readlane(
-                                                        __builtin_bit_cast(int, wf), src));
-          const float lw = __builtin_bit_cast(float, __builtin_amdgcn_readlane(
-                                                         __builtin_bit_cast(int, wl), src));
-          lsum[e % G] += lw;
-          acc0[e % G] += w * v[q][e][0];
-          acc1[e % G] += w * v[q][e][1];
-        }
-      }
+    for (int i = 0; i < 4; ++i) {
+      sc[i] = p * PAGE + slot0 + i < ke ? sacc[i] : -__builtin_inff();
+      mx = fmaxf(mx, sc[i]);
+    }
+    mx = max_xor32(max_xor16(mx));
+    const float m_tile = mx * c;
+    if (__builtin_amdgcn_ballot_w64(m_tile > m_run + RESCALE_LOG2)) {
+      const float m_new = m_tile > m_run + RESCALE_LOG2 ? m_tile : m_run;
+      const float alpha = fexp2(m_run - m_new);
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int mb = 0; mb < 8; ++mb) o[mb] *= alpha;
+    }
+    // P^T rounded to bf16: this lane's keys of its head column, the B operand.
+    u32x2_t pk;
+    pk[0] = pack_bf16(fexp2(__builtin_fmaf(sc[0], c, -m_run)),
+                      fexp2(__builtin_fmaf(sc[1], c, -m_run)));
+    pk[1] = pack_bf16(fexp2(__builtin_fmaf(sc[2], c, -m_run)),
+                      fexp2(__builtin_fmaf(sc[3], c, -m_run)));
+    constexpr uint32_t ONES = 0x3F803F80u;  // two bf16 1.0
+    l_run = dot2(pk[1], ONES, dot2(pk[0], ONES, l_run));
+    const s16x4_t pb = __builtin_bit_cast(s16x4_t, pk);
+    // O^T += V^T P^T, eight blocks of 16 dims.
+#pragma unroll
+    for (int mb = 0; mb < 8; ++mb) {
+      const s16x4_t vf = *reinterpret_cast<const s16x4_t*>(vl + mb * 512 + vbyte);
+      o[mb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vf, pb, o[mb], 0, 0, 0);
+    }
+    wave_sync();  // every lane done reading the slot before it is refilled
+    if (deep && p + 2 < p_end) issue(p + 2, slot);
+  };
+
+  for (int p = p_begin; p < p_end; p += 2) {
+    process(p, 0);
+    if (p + 1 < p_end) process(p + 1, 1);
+  }
+
+  // Row sums: each lane group holds a quarter of the keys of its head.
+  const float l_tot = sum_xor32(sum_xor16(l_run));
+  // o[mb][i] = O[head col][16 mb + 4 gq + i]
+  if (nsplits == 1) {
+    if (col < G) {
+      const float inv = 1.f / l_tot;
+      const int64_t orow = ((int64_t)tok * a.hq + kh * G + col) * D + 4 * gq;
+#pragma unroll
+      for (int mb = 0; mb < 8; ++mb)
+        store4(a, orow + 16 * mb, o[mb][0] * inv, o[mb][1] * inv, o[mb][2] * inv,
+               o[mb][3] * inv);
+    }
+    return ticket_v;
+  }
+
+  // Partial: O[G][128], m[G], l[G].
+  const int slot_floats = slot_floats_for(G);
+  const Slots sl = group_slots(a.ws, wsgroup, nsplits, slot_floats);
+  const int my = split * slot_floats;
+  if (col < G) {
+#pragma unroll
+    for (int mb = 0; mb < 8; ++mb) pstore4(sl, my + col * D + 16 * mb + 4 * gq, o[mb]);
+    if (gq == 0) {
+      pstore1(sl, my + G * D + col, m_run);
+      pstore1(sl, my + G * D + G + col, l_tot);
     }
   }
-#pragma unroll
-  for (int h = 0; h < G; ++h) {
-    const float inv = 1.f / lsum[h];
-    store2(a, obase + h * D, acc0[h] * inv, acc1[h] * inv);
-  }
-  if (lane == 0)
-    __hip_atomic_store(group_counter(a.ws, grp), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  wait_memory_complete();
+  int old = 0;
+  if (lane == 0) old = arrive(a.ws, grp);
+  old = __shfl(old, 0);
+  if (old != nsplits - 1) return ticket_v;
+  decode_merge<G>(a, sl, slot_floats, nsplits, ((int64_t)tok * a.hq + kh * G) * D + 2 * lane,
+                  grp);
   return ticket_v;
 }
 
@@ -1348,8 +1617,12 @@ __global__ __launch_bounds__(THREADS, 2) void attention_mixed_kernel(Args a) {
     if (queue && t >= a.decode_static) t = ticket();
     while (t < ndec) {
       // In queue mode the unit takes the next ticket itself near its end.
-      const int pending = decode_unit<G, APP>(
-          a, a.work + (int64_t)(a.num_prefill + t) * DLFP_WORK_INTS, wl, queue);
+      const int32_t* rec = a.work + (int64_t)(a.num_prefill + t) * DLFP_WORK_INTS;
+      int pending;
+      if constexpr (G >= 4)
+        pending = decode_unit_mfma<G, APP>(a, rec, wl, queue);
+      else
+        pending = decode_unit<G, APP>(a, rec, wl, queue);
       wave_sync();
       if (!queue) break;
       t = a.decode_static + uniform(__shfl(pending, 0));
