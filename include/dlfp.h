@@ -267,6 +267,30 @@ int dlfp_append_attention_mixed(const dlfp_dims* dims, const dlfp_meta* meta,
                                 void* v_cache, float scale, void* out, int32_t out_dtype,
                                 void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* For callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.
+ *
+ * dlfp_append_attention_mixed with the workspace taken from a fixed array of
+ * DLFP_STATIC_WORKSPACE_BYTES in device memory that the library holds, one
+ * copy per GPU, until the process ends; arguments otherwise as for that call
+ * (the caller still passes every input and output).  The call allocates
+ * nothing: no hipMalloc, no hipFree, no allocating library routine.  Its first
+ * call on a device looks up the array's address on that device and zeroes its
+ * header and counter region with a fill kernel on `stream`; every launch
+ * leaves them zero again.  All calls on one GPU share that GPU's array:
+ * calls that overlap on one GPU (on different streams, or from different
+ * threads without ordering) race on it and must not be made.
+ * Errors: DLFP_ENOSPC when meta->workspace_bytes exceeds
+ * DLFP_STATIC_WORKSPACE_BYTES (nothing is launched; a coarser split through
+ * dlfp_tuning needs less), otherwise as dlfp_append_attention_mixed. */
+#define DLFP_STATIC_WORKSPACE_BYTES (128u << 20)
+int dlfp_append_attention_mixed_static(const dlfp_dims* dims, const dlfp_meta* meta,
+                                       const int32_t* d_work, const int32_t* d_block_table,
+                                       int32_t max_blocks, int32_t num_blocks, const void* q,
+                                       const void* k_new, const void* v_new, void* k_cache,
+                                       void* v_cache, float scale, void* out, int32_t out_dtype,
+                                       hipStream_t stream);
+
 /* Zero the workspace header and the whole counter region (the first
  * DLFP_WORKSPACE_PARTIALS bytes) with a stream-ordered fill kernel.  Needed
  * once per workspace allocation.  DLFP_ENOSPC if workspace_bytes is smaller. */

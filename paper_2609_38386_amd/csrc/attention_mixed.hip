@@ -45,6 +45,7 @@
 
 #include <algorithm>
 #include <cstdint>
+#include <mutex>
 #include <type_traits>
 
 #include "dlfp.h"
@@ -1643,6 +1644,13 @@ __global__ __launch_bounds__(THREADS, 2) void attention_mixed_kernel(Args a) {
   }
 }
 
+// Workspace of dlfp_append_attention_mixed_static: a fixed array in device
+// memory, one copy per GPU the library runs on, held until the process ends.
+// Host code must not pass the array's name to a kernel (on the host it only
+// stands for the symbol); static_workspace() below looks up its device address
+// once per device.
+__device__ __align__(256) char scratch[DLFP_STATIC_WORKSPACE_BYTES];
+
 __global__ void fill_zero_kernel(int* p, int64_t n) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) p[i] = 0;
@@ -1762,6 +1770,28 @@ int launch_mixed(const dlfp_dims* dims, const dlfp_meta* meta, const int32_t* d_
   return e == hipSuccess ? DLFP_OK : DLFP_EHIP;
 }
 
+// Device address of `scratch` on the current device, looked up (and its
+// header and counter region zeroed by a fill kernel on `stream`) on the first
+// call for that device.  Launches leave the header and counters zero again.
+int static_workspace(void** ptr, hipStream_t stream) {
+  static std::mutex mu;
+  static void* addr[64] = {nullptr};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return DLFP_EHIP;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return DLFP_EHIP;
+    const int64_t n = DLFP_WORKSPACE_PARTIALS / 4;
+    (void)hipGetLastError();
+    fill_zero_kernel<<<(unsigned)((n + 255) / 256), 256, 0, stream>>>(static_cast<int*>(p), n);
+    if (hipGetLastError() != hipSuccess) return DLFP_EHIP;
+    addr[dev] = p;
+  }
+  *ptr = addr[dev];
+  return DLFP_OK;
+}
+
 }  // namespace
 
 extern "C" int dlfp_attention_mixed(const dlfp_dims* dims, const dlfp_meta* meta,
@@ -1787,6 +1817,24 @@ extern "C" int dlfp_append_attention_mixed(const dlfp_dims* dims, const dlfp_met
   return launch_mixed(dims, meta, d_work, d_block_table, max_blocks, num_blocks, q, k_new,
                       v_new, k_cache, v_cache, scale, out, out_dtype, workspace,
                       workspace_bytes, stream);
+}
+
+extern "C" int dlfp_append_attention_mixed_static(const dlfp_dims* dims, const dlfp_meta* meta,
+                                                  const int32_t* d_work,
+                                                  const int32_t* d_block_table,
+                                                  int32_t max_blocks, int32_t num_blocks,
+                                                  const void* q, const void* k_new,
+                                                  const void* v_new, void* k_cache,
+                                                  void* v_cache, float scale, void* out,
+                                                  int32_t out_dtype, hipStream_t stream) {
+  if (!k_new || !v_new || !meta) return DLFP_EINVAL;
+  if (meta->workspace_bytes > (int64_t)DLFP_STATIC_WORKSPACE_BYTES) return DLFP_ENOSPC;
+  void* ws = nullptr;
+  const int st = static_workspace(&ws, stream);
+  if (st != DLFP_OK) return st;
+  return launch_mixed(dims, meta, d_work, d_block_table, max_blocks, num_blocks, q, k_new, v_new,
+                      k_cache, v_cache, scale, out, out_dtype, ws, DLFP_STATIC_WORKSPACE_BYTES,
+                      stream);
 }
 
 extern "C" int dlfp_workspace_init(void* workspace, size_t workspace_bytes, hipStream_t stream) {

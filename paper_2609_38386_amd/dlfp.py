@@ -67,7 +67,7 @@ class dlfp_controller(ctypes.Structure):
 
 
 EXPORTS = ["dlfp_build_varlen_meta", "dlfp_kv_append", "dlfp_attention_mixed",
-           "dlfp_append_attention_mixed",
+           "dlfp_append_attention_mixed", "dlfp_append_attention_mixed_static",
            "dlfp_workspace_init", "dlfp_workspace_error", "dlfp_controller_init",
            "dlfp_controller_step", "dlfp_timer_create", "dlfp_timer_destroy", "dlfp_timer_start",
            "dlfp_timer_stop", "dlfp_timer_elapsed_ms", "dlfp_stream_hold", "dlfp_status_string",
@@ -99,6 +99,10 @@ def lib():
                                               ctypes.POINTER(dlfp_meta), vp, vp, i32, i32, vp,
                                               vp, vp, vp, vp, ctypes.c_float, vp, i32, vp, sz,
                                               vp]
+    L.dlfp_append_attention_mixed_static.argtypes = [ctypes.POINTER(dlfp_dims),
+                                                     ctypes.POINTER(dlfp_meta), vp, vp, i32, i32,
+                                                     vp, vp, vp, vp, vp, ctypes.c_float, vp, i32,
+                                                     vp]
     L.dlfp_workspace_init.argtypes = [vp, sz, vp]
     L.dlfp_workspace_error.argtypes = [vp, _P32, vp]
     L.dlfp_controller_init.argtypes = [ctypes.POINTER(dlfp_controller), ctypes.c_double, i32, i32,
@@ -240,6 +244,23 @@ def dlfp_append_attention_mixed(dims: dlfp_dims, meta: Meta, d_work, d_block_tab
         _dptr(v_new), _dptr(k_cache), _dptr(v_cache), float(scale), _dptr(out), out_dtype,
         _dptr(workspace), int(workspace.numel() * workspace.element_size()), _stream(stream))
     _check(st, "dlfp_append_attention_mixed")
+
+
+STATIC_WORKSPACE_BYTES = 128 << 20
+
+
+def dlfp_append_attention_mixed_static(dims: dlfp_dims, meta: Meta, d_work, d_block_table, q,
+                                       k_new, v_new, k_cache, v_cache, scale: float, out,
+                                       stream=None) -> None:
+    """dlfp_append_attention_mixed on the library's own device workspace (no allocation)."""
+    import torch
+    out_dtype = {torch.bfloat16: 0, torch.float32: 1}[out.dtype]
+    st = lib().dlfp_append_attention_mixed_static(
+        ctypes.byref(dims), ctypes.byref(meta.c), _dptr(d_work), _dptr(d_block_table),
+        int(d_block_table.shape[1]), int(k_cache.shape[0]), _dptr(q), _dptr(k_new),
+        _dptr(v_new), _dptr(k_cache), _dptr(v_cache), float(scale), _dptr(out), out_dtype,
+        _stream(stream))
+    _check(st, "dlfp_append_attention_mixed_static")
 
 
 def dlfp_workspace_init(workspace, stream=None) -> None:
