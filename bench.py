@@ -556,12 +556,56 @@ def run_overlap_replay(dev, seed, rate, log_fn):
     caps = [it["limit"] for it in trace if it["guarded"]]
     lag = rp.run_replay(cfg, rp.Policy(rp.Policy.DLFP_LAG1, target_ms=target, cfg=cfg), ex)
     out = {"seed": seed, "rate_per_s": rate, "target_layer_ms": round(target, 5),
-           "guarded_cap_p50": int(np.median(caps)) if caps else None}
+           "guarded_cap_p50": int(np.median(caps)) if caps else None,
+           "guarded_cycles_at_c_min": (round(float(np.mean(np.asarray(caps) == cfg.c_min)), 4)
+                                       if caps else None)}
     for name, r in (("uncapped", base), ("dlfp", dl), ("dlfp_lag1", lag)):
         out[name] = {k: (round(r[k], 4) if isinstance(r[k], float) else r[k]) for k in keys}
     log_fn(f"overlap replay {rate} req/s: {time.time() - t0:.1f}s, controlled L/T p50 "
            f"{dl['controlled_L_over_T_p50']}, within 5% {dl['controlled_within_5pct']}")
     del ex
+    return out
+
+
+def run_root_cause_replays(dev, seed, rates, log_fn):
+    """The paper's failure mode (Sec. 3.2, Sec. 6.3, Sec. 6.4) on the device: the
+    replay with an engine pipeline whose scheduler calls cost the host time
+    measured for them.  Asynchronous scheduling (the scheduler one iteration
+    ahead): uncapped, Eq. 2 on the completion time as it becomes available (one
+    iteration late) and Eq. 2 on the interval between scheduler calls.
+    Synchronous scheduling: uncapped, Eq. 2 on the completion time, and the
+    completion-aware revision (host time from the call to the returned output,
+    each step bounded to a factor of two).  Reported with how far each signal was
+    from the guarded cycle's device time and how often it moved the cap the
+    wrong way."""
+    from paper_2609_38386_amd import replay as rp
+    keys = ("itl_p50_ms", "itl_p99_ms", "ttft_p50_ms", "ttft_p99_ms", "iterations",
+            "guarded_iterations", "controlled_iterations", "controlled_L_over_T_p50",
+            "controlled_L_over_T_p90", "controlled_within_5pct", "signal_rel_error_mean",
+            "wrong_direction_updates", "reconciled")
+    out = {}
+    for rate in rates:
+        for pipe, kinds in (("async", (rp.Policy.DLFP_LAG1, rp.Policy.DLFP_CADENCE)),
+                            ("sync", (rp.Policy.DLFP, rp.Policy.DLFP_REVISED))):
+            cfg = rp.ReplayConfig(seed=seed, rate_per_s=rate, pipeline=pipe)
+            ex = rp.GpuExecutor(cfg, dev)
+            t0 = time.time()
+            trace = []
+            runs = {"uncapped": rp.run_replay(cfg, rp.Policy(rp.Policy.UNCAPPED), ex, trace=trace)}
+            target = 1.2 * float(np.median([it["layer_ms"] for it in trace
+                                            if it["decoders"] > 0 and it["p_t"] == 0]))
+            for k in kinds:
+                runs[k] = rp.run_replay(cfg, rp.Policy(k, target_ms=target, cfg=cfg), ex)
+            rec = {"target_layer_ms": round(target, 5)}
+            for name, r in runs.items():
+                rec[name] = {k: (round(r[k], 4) if isinstance(r[k], float) else r[k])
+                             for k in keys}
+            out[f"{pipe}_{rate:g}_req_s"] = rec
+            log_fn(f"root-cause replay {pipe} {rate} req/s: {time.time() - t0:.1f}s, p99 ITL "
+                   + ", ".join(f"{n} {r['itl_p99_ms']:.3f}" for n, r in runs.items()))
+            del ex
+    out["note"] = ("clock = device completion times of a pipeline whose scheduler calls cost the "
+                   "host time measured for them; signals per layer (x28 layers)")
     return out
 
 
@@ -731,6 +775,7 @@ def main():
         seeds = [int(x) for x in args.replay_seeds.split(",")]
         replay = run_replays(dev, seeds, logf)
         replay["overlap_20_req_s"] = run_overlap_replay(dev, seeds[0], 20.0, logf)
+        replay["root_cause"] = run_root_cause_replays(dev, seeds[0], (2.0, 20.0), logf)
     if any(errors.values()):
         print(f"bench.py: the workspace error word is set after the timed launches: {errors} "
               "(1 = a block id outside the pool, 2 = a wait for the append records ran out); "

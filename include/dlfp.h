@@ -23,8 +23,14 @@
  *
  * Conventions for every call:
  *  - Return value: DLFP_OK (0) or a negative dlfp_status.  No call throws,
- *    aborts, prints, or synchronises a stream.  Validation happens before any
- *    launch; on error nothing is launched and no output is written.
+ *    aborts or prints.  No call synchronises a stream except two, by design:
+ *    dlfp_timer_elapsed_ms waits for its stop event (completion timing) and
+ *    dlfp_workspace_error synchronises the stream before reading the error
+ *    word.  Every argument is validated before anything is launched; on a
+ *    validation error nothing is launched and no output is written.  A
+ *    DLFP_EHIP from a launch that follows another launch of the same call
+ *    (only dlfp_append_attention_mixed with more than 128 append records,
+ *    see there) leaves the first launch's work enqueued.
  *  - Ownership: the caller owns every buffer (device and host).  The library
  *    allocates no device memory and keeps no pointer after returning.
  *  - Device calls are stream-ordered and asynchronous; a device-side fault
@@ -259,7 +265,11 @@ int dlfp_attention_mixed(const dlfp_dims* dims, const dlfp_meta* meta, const int
  * units to finish zeroes the words again.  When the records would need more
  * than 16 such workgroups (above 128 records), they are written by a launch
  * of their own just before, and the prefill units do not wait.
- * Errors: as dlfp_attention_mixed. */
+ * Errors: as dlfp_attention_mixed.  With more than 128 append records, a
+ * DLFP_EHIP reported for the attention launch can follow a successful enqueue
+ * of the append-records launch: the cache may then hold the iteration's new
+ * keys and values although the call failed (every argument is checked before
+ * either launch, so only a runtime launch failure leads there). */
 int dlfp_append_attention_mixed(const dlfp_dims* dims, const dlfp_meta* meta,
                                 const int32_t* d_work, const int32_t* d_block_table,
                                 int32_t max_blocks, int32_t num_blocks, const void* q,

@@ -31,6 +31,7 @@ from __future__ import annotations
 
 import dataclasses
 import math
+import time
 from typing import Callable, Dict, List, Optional, Sequence
 
 import numpy as np
@@ -98,6 +99,15 @@ class ReplayConfig:
     c_min: int = 32
     c_max: int = 4096
     quantum: int = 128
+    # Engine pipeline (Sec. 3.2, Sec. 6.4).  None: the clock advances by `layers`
+    # x the measured one-layer device latency and host time is left out.
+    # "sync": each scheduler call waits for the previous iteration's output;
+    # "async": the scheduler prepares iteration t + 1 while t runs (at most one
+    # iteration ahead of the device).  In both modes a scheduler call costs
+    # `host_ms` of host time (None: the host time the replay measures for the
+    # call, batch formation plus the executor's preparation of its launches).
+    pipeline: Optional[str] = None
+    host_ms: Optional[float] = None
 
     @property
     def max_blocks(self) -> int:
@@ -112,11 +122,27 @@ class Policy:
 
     UNCAPPED = "uncapped"
     FIXED = "fixed"
+    # Eq. 2 on the iteration's device completion time (HIP events).
     DLFP = "dlfp"
     # Eq. 2 fed one iteration late: an asynchronous engine that sets the cap of
     # iteration t + 1 while iteration t still runs only has the completion time
     # of iteration t - 1 (the stale signal of Sec. 6.4).
     DLFP_LAG1 = "dlfp_lag1"
+    # Eq. 2 on the interval between scheduler calls (the prototype's signal,
+    # Sec. 3.2); under asynchronous scheduling the interval that follows a
+    # guarded cycle is set by the host and by earlier queued work, not by that
+    # cycle's device time (Sec. 6.4).
+    DLFP_CADENCE = "dlfp_cadence"
+    # The completion-aware revision (Sec. 6.3): the update happens when the
+    # scheduler's output for the cycle returns (host time from the scheduler
+    # call to the returned output) and each control step is bounded; read here
+    # as the cap changing by at most a factor of two per update, i.e. Eq. 2 on
+    # the observation clamped to [T / 2, 2 T].
+    DLFP_REVISED = "dlfp_revised"
+
+    SIGNAL = {DLFP: "device", DLFP_LAG1: "device", DLFP_CADENCE: "cadence",
+              DLFP_REVISED: "returned"}
+    STEP_BOUND = 2.0
 
     def __init__(self, kind: str, cap: int = 0, target_ms: float = 0.0, cfg: ReplayConfig = None):
         self.kind = kind
@@ -124,7 +150,7 @@ class Policy:
         self.target_ms = target_ms
         self.ctrl = None
         self.pending = None       # DLFP_LAG1: the observation not yet delivered
-        if kind in (self.DLFP, self.DLFP_LAG1):
+        if kind in self.SIGNAL:
             from . import dlfp as D
             self._D = D
             self.ctrl = D.dlfp_controller_init(target_ms, cfg.c_initial, cfg.c_min, cfg.c_max,
@@ -133,6 +159,7 @@ class Policy:
         # True when the next cycle's cap comes from a feedback update (Eq. 2)
         # rather than from c_initial after a reset.
         self.controlled = False
+        self.last_observed = None   # the observation of the latest guarded update
 
     def limit(self, n_decoding: int, budget: int) -> int:
         if n_decoding == 0 or self.kind == self.UNCAPPED:
@@ -142,19 +169,28 @@ class Policy:
         cap = self.next_cap if self.next_cap > 0 else self.ctrl.cap
         return min(cap, budget)
 
-    def observe(self, n_decoding_next: int, guarded: bool, observed_ms: float):
+    def observe(self, n_decoding_next: int, guarded: bool, signals: Dict[str, float]):
+        """`signals`: per-layer ms of the cycle that just ran -- 'device' (its HIP
+        event time), and in pipeline replays 'cadence' (scheduler-call interval that
+        follows it) and 'returned' (scheduler call to returned output)."""
+        if self.kind not in self.SIGNAL:
+            return
+        observed_ms = signals[self.SIGNAL[self.kind]]
         if self.kind == self.DLFP_LAG1:
             # this iteration's completion is delivered one call later; the
             # previous one's arrives now (nothing before the first completion)
             prev, self.pending = self.pending, (guarded, observed_ms)
             guarded, observed_ms = prev if prev is not None else (False, observed_ms)
-        if self.kind in (self.DLFP, self.DLFP_LAG1):
-            if guarded:
-                self.controlled = True
-            elif n_decoding_next == 0:
-                self.controlled = False
-            self.next_cap = self._D.dlfp_controller_step(self.ctrl, n_decoding_next, guarded,
-                                                         observed_ms)
+        if self.kind == self.DLFP_REVISED:
+            t = self.target_ms
+            observed_ms = min(max(observed_ms, t / self.STEP_BOUND), t * self.STEP_BOUND)
+        if guarded:
+            self.controlled = True
+            self.last_observed = observed_ms
+        elif n_decoding_next == 0:
+            self.controlled = False
+        self.next_cap = self._D.dlfp_controller_step(self.ctrl, n_decoding_next, guarded,
+                                                     observed_ms)
 
 
 Executor = Callable[[np.ndarray, np.ndarray, np.ndarray], float]
@@ -162,7 +198,21 @@ Executor = Callable[[np.ndarray, np.ndarray, np.ndarray], float]
 
 def run_replay(cfg: ReplayConfig, policy: Policy, execute: Executor,
                trace: Optional[list] = None, requests_out: Optional[list] = None) -> Dict:
-    """Run the replay; ``execute(q_len, kv_len, block_table) -> one-layer ms``."""
+    """Run the replay; ``execute(q_len, kv_len, block_table) -> one-layer ms``.
+
+    Time.  Without a pipeline (``cfg.pipeline is None``) an iteration takes
+    ``layers`` x its measured one-layer latency and the scheduler runs at its
+    completion.  With one, scheduler call t happens at S_t and costs h host ms;
+    the device starts the iteration when the host has enqueued it and the
+    previous iteration has completed, and completes it ``layers`` x its latency
+    later (C_t); the next call comes at max(S_t + h, C_t) ("sync") or at
+    max(S_t + h, C_{t-1}) ("async", one iteration ahead).  Tokens are produced
+    at completion times: a decoder's inter-token latency is the gap between its
+    consecutive tokens, time to first token runs from arrival to the completion
+    of the iteration that finishes the prompt.
+    """
+    if cfg.pipeline not in (None, "sync", "async"):
+        raise ValueError(f"unknown pipeline {cfg.pipeline!r}")
     arrivals = wl.poisson_arrivals(cfg.seed, cfg.n_requests, cfg.rate_per_s)
     prompts = wl.prompt_lengths(cfg.seed, cfg.n_requests, cfg.prompt_lo, cfg.prompt_hi)
     reqs = [Request(i, float(arrivals[i]), int(prompts[i]), cfg.out_len)
@@ -170,16 +220,20 @@ def run_replay(cfg: ReplayConfig, policy: Policy, execute: Executor,
     if requests_out is not None:
         requests_out.extend(reqs)
     alloc = PageAllocator(cfg.num_blocks(), cfg.seed)
-    clock = 0.0
+    now = 0.0                    # time of the next scheduler call (s)
+    c_prev = 0.0                 # completion time of the previous iteration (s)
+    last_token = {}              # request id -> time of its latest token
     nxt = 0                      # next request to arrive
     active: List[Request] = []   # arrived and not finished, in arrival order
     iterations = guarded_n = 0
     guarded_ratio = []
     controlled_ratio = []   # guarded cycles whose cap came from a feedback update
+    misjudged = []          # guarded updates: (observation, device latency)
     while nxt < len(reqs) or active:
+        t_call = time.perf_counter()
         if not active:
-            clock = max(clock, reqs[nxt].arrival_s)
-        while nxt < len(reqs) and reqs[nxt].arrival_s <= clock:
+            now = max(now, reqs[nxt].arrival_s)
+        while nxt < len(reqs) and reqs[nxt].arrival_s <= now:
             active.append(reqs[nxt])
             nxt += 1
         decoders = [r for r in active if r.decoding][:cfg.max_seqs]
@@ -211,21 +265,35 @@ def run_replay(cfg: ReplayConfig, policy: Policy, execute: Executor,
         for i, pages in enumerate(rows):
             bt[i, :len(pages)] = pages
         controlled = policy.controlled
+        host_sched_ms = (time.perf_counter() - t_call) * 1e3
         ms = float(execute(np.asarray(q_len, np.int32), np.asarray(kv_len, np.int32), bt))
         iter_ms = cfg.layers * ms
-        clock += iter_ms * 1e-3
+        signals = {"device": ms}
+        if cfg.pipeline is None:
+            done = now + iter_ms * 1e-3
+            now_next = done
+        else:
+            h = cfg.host_ms if cfg.host_ms is not None else (
+                host_sched_ms + float(getattr(execute, "last_host_ms", 0.0)))
+            enq = now + h * 1e-3
+            done = max(enq, c_prev) + iter_ms * 1e-3
+            now_next = max(enq, done if cfg.pipeline == "sync" else c_prev)
+            signals["cadence"] = (now_next - now) * 1e3 / cfg.layers
+            signals["returned"] = (done - now) * 1e3 / cfg.layers
         iterations += 1
         for r, take in slices:
             r.prefilled += take
             if r.prefilled == r.prompt_len:
                 r.generated = 1
-                r.first_token_s = clock
+                r.first_token_s = done
+                last_token[r.rid] = done
         for r in decoders:
             r.generated += 1
-            r.itl_ms.append(iter_ms)
+            r.itl_ms.append((done - last_token[r.rid]) * 1e3)
+            last_token[r.rid] = done
         for r in list(active):
             if r.generated >= r.out_len:
-                r.done_s = clock
+                r.done_s = done
                 alloc.release(r)
                 active.remove(r)
         n_next = sum(1 for r in active if r.decoding)
@@ -235,14 +303,21 @@ def run_replay(cfg: ReplayConfig, policy: Policy, execute: Executor,
                 guarded_ratio.append(ms / policy.target_ms)
                 if controlled:
                     controlled_ratio.append(ms / policy.target_ms)
-        policy.observe(n_next, guarded, ms)
+        policy.observe(n_next, guarded, signals)
+        if guarded and policy.last_observed is not None and policy.kind != Policy.DLFP_LAG1:
+            misjudged.append((policy.last_observed, ms))
         if trace is not None:
-            trace.append({"t": round(clock, 6), "decoders": len(decoders), "p_t": p_t,
-                          "limit": limit, "layer_ms": round(ms, 5), "guarded": guarded})
+            trace.append({"t": round(done, 6), "decoders": len(decoders), "p_t": p_t,
+                          "limit": limit, "layer_ms": ms, "guarded": guarded,
+                          "signals": signals})
+        c_prev = done
+        now = now_next
     itl = np.concatenate([np.asarray(r.itl_ms) for r in reqs if r.itl_ms] or [np.zeros(0)])
     ttft = np.asarray([(r.first_token_s - r.arrival_s) * 1e3 for r in reqs])
     e2e = np.asarray([(r.done_s - r.arrival_s) * 1e3 for r in reqs])
     reconciled = reconcile(reqs)
+    obs = np.asarray(misjudged) if misjudged else np.zeros((0, 2))
+    tgt = policy.target_ms or 1.0
     return {
         "iterations": iterations,
         "guarded_iterations": guarded_n,
@@ -264,6 +339,13 @@ def run_replay(cfg: ReplayConfig, policy: Policy, execute: Executor,
                                     if controlled_ratio else None),
         "controlled_L_over_T_p90": (float(np.percentile(controlled_ratio, 90))
                                     if controlled_ratio else None),
+        # How far the controller's observation was from the guarded cycle's device
+        # time, and how often it pointed the cap the wrong way (observation and
+        # device time on opposite sides of the target).
+        "signal_rel_error_mean": (float(np.mean(np.abs(obs[:, 0] - obs[:, 1]) / obs[:, 1]))
+                                  if len(obs) else None),
+        "wrong_direction_updates": (float(np.mean((obs[:, 0] <= tgt) != (obs[:, 1] <= tgt)))
+                                    if len(obs) else None),
         "reconciled": reconciled,
         "prompt_tokens": int(sum(r.prompt_len for r in reqs)),
         "output_tokens": int(sum(r.generated for r in reqs)),
@@ -321,9 +403,11 @@ class GpuExecutor:
         self.timer = D.Timer()
         self.scale = 1.0 / math.sqrt(128)
         self.hold_us = 150
+        self.last_host_ms = 0.0
 
     def __call__(self, q_len: np.ndarray, kv_len: np.ndarray, bt: np.ndarray) -> float:
         D = self.D
+        t0 = time.perf_counter()
         st = self.stage.build(q_len, kv_len, bt, self.num_blocks)
         n = bt.size
         self.bt_host.numpy()[:n] = bt.reshape(-1)
@@ -333,6 +417,8 @@ class GpuExecutor:
         ws = self.ws.ensure(st.meta.workspace_bytes)
         # Launch marshalling happens while the stream idles, so the events bracket
         # the layer's device work and not the host's launch gaps.
+        # host time of preparing the iteration's launches (metadata, staging)
+        self.last_host_ms = (time.perf_counter() - t0) * 1e3
         D.dlfp_stream_hold(self.hold_us)
         self.timer.start()
         D.dlfp_append_attention_mixed(self.dims, st.meta, st.d_work, d_bt, self.q[:T],

@@ -1,12 +1,28 @@
 """Replay on the device: the scheduler drives the real append + single attention launch
 and the controller reads HIP-event completion times.  Latencies are parity unpinned
-(they depend on the GPU); reconciliation and the controller's guard are checked."""
+(they depend on the GPU); reconciliation, the controller's guard and every control
+decision are checked: the recorded latency trace, replayed through the oracle's Eq. 2
+controller, must give the same cap before every iteration."""
 import pytest
 import torch
 
+from oracle import controller as oc
 from paper_2609_38386_amd import replay as rp
 
 pytestmark = pytest.mark.gpu
+
+
+def expected_limits(trace, cfg, target):
+    """Prefill limit of every iteration after the first, from the oracle controller fed
+    the trace's guarded flags and measured latencies (C3/C4: update after a guarded
+    cycle, reset when the next cycle has no decoder)."""
+    ctrl = oc.Controller(target, cfg.c_initial, cfg.c_min, cfg.c_max, cfg.quantum)
+    out = []
+    for prev, nxt in zip(trace, trace[1:]):
+        cap = ctrl.step(nxt["decoders"], prev["guarded"], prev["layer_ms"])
+        budget = cfg.budget - nxt["decoders"]
+        out.append(budget if cap == oc.UNCAPPED else min(cap, budget))
+    return out
 
 
 def test_gpu_replay_uncapped_and_dlfp():
@@ -26,3 +42,8 @@ def test_gpu_replay_uncapped_and_dlfp():
     assert dl["reconciled"]
     assert all(it["limit"] == cfg.budget for it in trace2 if it["decoders"] == 0)
     assert dl["guarded_iterations"] > 0
+    # every decision equals the oracle controller's on the recorded latencies
+    want = expected_limits(trace2, cfg, target)
+    got = [it["limit"] for it in trace2[1:]]
+    assert got == want
+    assert len(set(got)) > 2   # the cap moved

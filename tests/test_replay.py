@@ -122,3 +122,76 @@ def test_stale_completion_signal_holds_the_target_worse():
     assert lag["reconciled"] and lag["controlled_iterations"] > 0
     assert lag["itl_p99_ms"] >= dl["itl_p99_ms"]
     assert lag["controlled_within_5pct"] < dl["controlled_within_5pct"]
+
+
+def _overlap_cfg(**kw):
+    return _cfg(n_requests=40, rate_per_s=300.0, out_len=32, **kw)
+
+
+def test_cadence_signal_misjudges_the_device_latency_under_async_scheduling():
+    """Sec. 3.2 / Sec. 6.4: with the scheduler one iteration ahead of the device,
+    the interval between scheduler calls that follows a guarded cycle is set by
+    the host's own cost and by the iteration queued before it, not by the
+    guarded cycle's device time.  Fed to Eq. 2, it moves the cap the wrong way
+    on many updates (expanding it after a short interval while a long chunk is
+    still running), and the decoders' tail latency comes back close to the
+    uncapped one; the completion time, delivered when it is available (one
+    iteration late under this scheduling), keeps most of the reduction."""
+    cfg = _overlap_cfg(pipeline="async", host_ms=0.3)
+    model = rp.linear_latency_model(0.01, 2e-5, 2e-4)
+    base = rp.run_replay(cfg, rp.Policy(rp.Policy.UNCAPPED), model)
+    comp = rp.run_replay(cfg, rp.Policy(rp.Policy.DLFP_LAG1, target_ms=0.03, cfg=cfg), model)
+    cad = rp.run_replay(cfg, rp.Policy(rp.Policy.DLFP_CADENCE, target_ms=0.03, cfg=cfg), model)
+    assert base["reconciled"] and comp["reconciled"] and cad["reconciled"]
+    assert cad["signal_rel_error_mean"] > 0.3
+    assert cad["wrong_direction_updates"] > 0.3
+    assert cad["itl_p99_ms"] > 1.3 * comp["itl_p99_ms"]
+    assert cad["itl_p99_ms"] > 0.8 * base["itl_p99_ms"]
+    assert cad["controlled_within_5pct"] < comp["controlled_within_5pct"]
+    assert comp["itl_p99_ms"] < 0.7 * base["itl_p99_ms"]
+
+
+def test_cadence_equals_completion_when_the_host_is_synchronous_and_free():
+    """With a synchronous scheduler and no host cost, the interval between calls
+    is exactly the iteration's completion time: the two signals coincide."""
+    cfg = _overlap_cfg(pipeline="sync", host_ms=0.0)
+    model = rp.linear_latency_model(0.01, 2e-5, 2e-4)
+    t1, t2 = [], []
+    a = rp.run_replay(cfg, rp.Policy(rp.Policy.DLFP, target_ms=0.03, cfg=cfg), model, trace=t1)
+    b = rp.run_replay(cfg, rp.Policy(rp.Policy.DLFP_CADENCE, target_ms=0.03, cfg=cfg), model,
+                      trace=t2)
+    assert [x["limit"] for x in t1] == [x["limit"] for x in t2]
+    assert a["itl_p99_ms"] == b["itl_p99_ms"]
+    assert b["signal_rel_error_mean"] < 1e-9
+    # with no host cost and no pipelining the clock is the device time alone
+    plain = rp.run_replay(_overlap_cfg(), rp.Policy(rp.Policy.DLFP, target_ms=0.03,
+                                                    cfg=_overlap_cfg()), model)
+    assert plain["itl_p99_ms"] == pytest.approx(a["itl_p99_ms"])
+
+
+def test_completion_aware_revision_bounds_each_step():
+    """Sec. 6.3: the revised controller updates when the cycle's output returns
+    (host time from the scheduler call, so the host's own cost is counted) and
+    changes the cap by at most a factor of two per update.  Under synchronous
+    scheduling it keeps the tail inter-token latency low but, with the host cost
+    counted as device latency, pins the cap near its floor and multiplies the
+    time to first token (it moves latency rather than removing it)."""
+    cfg = _overlap_cfg(pipeline="sync", host_ms=0.3)
+    model = rp.linear_latency_model(0.01, 2e-5, 2e-4)
+    trace = []
+    rev = rp.run_replay(cfg, rp.Policy(rp.Policy.DLFP_REVISED, target_ms=0.03, cfg=cfg), model,
+                        trace=trace)
+    base = rp.run_replay(cfg, rp.Policy(rp.Policy.UNCAPPED), model)
+    assert rev["reconciled"]
+    caps = [x["limit"] for x in trace if x["decoders"] > 0]
+    steps = [(a, b) for a, b in zip(caps, caps[1:]) if a <= cfg.c_max and b <= cfg.c_max]
+    assert steps
+    for a, b in steps:
+        assert b <= 2 * a
+        assert b >= min(a, max(cfg.c_min, (a // 2) // cfg.quantum * cfg.quantum))
+    assert rev["itl_p99_ms"] < base["itl_p99_ms"]
+    assert rev["ttft_p99_ms"] > 3 * base["ttft_p99_ms"]
+    # the bound is a clamp of the observation to [T / 2, 2 T] before Eq. 2
+    pol = rp.Policy(rp.Policy.DLFP_REVISED, target_ms=0.03, cfg=cfg)
+    pol.observe(3, True, {"returned": 10.0})
+    assert pol.ctrl.cap == cfg.c_initial // 2 // 128 * 128
