@@ -56,6 +56,8 @@ def parse_args():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--replay-seeds", default="801,802,803",
                     help="seeds of the closed-loop replay (comma list, or 'none')")
+    ap.add_argument("--variant-requests", type=int, default=24,
+                    help="requests per workload-variant replay")
     ap.add_argument("--quiet", action="store_true")
     ap.add_argument("--two-launch", action="store_true",
                     help="append with dlfp_kv_append, then dlfp_attention_mixed (instead of "
@@ -609,6 +611,93 @@ def run_root_cause_replays(dev, seed, rates, log_fn):
     return out
 
 
+REPLAY_KEYS = ("itl_p50_ms", "itl_p99_ms", "ttft_p50_ms", "ttft_p99_ms", "e2e_p99_ms",
+               "iterations", "guarded_iterations", "controlled_iterations",
+               "controlled_L_over_T_p50", "controlled_L_over_T_p90", "controlled_within_target",
+               "controlled_within_5pct", "reconciled")
+
+
+def paired_replay(cfg, dev, log_fn, label):
+    """Uncapped, then DLFP with the target at 1.2x the uncapped run's median
+    decode-only latency; the guarded caps' distribution and the P99 ITL change."""
+    from paper_2609_38386_amd import replay as rp
+    ex = rp.GpuExecutor(cfg, dev)
+    t0 = time.time()
+    trace = []
+    base = rp.run_replay(cfg, rp.Policy(rp.Policy.UNCAPPED), ex, trace=trace)
+    dec = [it["layer_ms"] for it in trace if it["decoders"] > 0 and it["p_t"] == 0]
+    target = 1.2 * float(np.median(dec))
+    chunk_ms = [(it["p_t"], it["layer_ms"]) for it in trace if it["p_t"] > 0]
+    trace = []
+    dl = rp.run_replay(cfg, rp.Policy(rp.Policy.DLFP, target_ms=target, cfg=cfg), ex, trace=trace)
+    caps = np.asarray([it["limit"] for it in trace if it["guarded"]])
+    rec = {"target_layer_ms": round(target, 5),
+           "decode_only_layer_ms_p50": round(float(np.median(dec)), 5)}
+    if len({p for p, _ in chunk_ms}) >= 2:
+        pt, ms = np.asarray(chunk_ms, dtype=np.float64).T
+        slope, icpt = np.polyfit(pt, ms, 1)
+        rec["layer_ms_vs_p_t_fit"] = {"intercept_ms": round(float(icpt), 5),
+                                      "ms_per_1k_tokens": round(float(slope) * 1e3, 5)}
+    for name, r in (("uncapped", base), ("dlfp", dl)):
+        rec[name] = {k: (round(r[k], 4) if isinstance(r[k], float) else r[k]) for k in REPLAY_KEYS}
+    rec["p99_itl_reduction_pct"] = round(
+        100.0 * (base["itl_p99_ms"] - dl["itl_p99_ms"]) / base["itl_p99_ms"], 2)
+    if len(caps):
+        rec["guarded_caps"] = {"p10": int(np.percentile(caps, 10)), "p50": int(np.median(caps)),
+                               "p90": int(np.percentile(caps, 90)),
+                               "at_c_min": round(float(np.mean(caps == cfg.c_min)), 4)}
+    log_fn(f"{label}: {time.time() - t0:.1f}s, p99 ITL {base['itl_p99_ms']:.3f} -> "
+           f"{dl['itl_p99_ms']:.3f} ms, guarded {dl['guarded_iterations']}")
+    del ex
+    return rec
+
+
+def run_layer_proxy_replays(dev, seeds, log_fn):
+    """The replay of config 2 with the full-iteration proxy (Eq. 1's linear
+    term): the layer's projections timed with the attention, so the iteration
+    latency grows with p_t and Eq. 2 regulates instead of clamping at c_min.
+    Paired per seed at 2 req/s, plus seed 801 at 20 req/s."""
+    from paper_2609_38386_amd import replay as rp
+    out = {"per_seed": {}}
+    reds = []
+    for seed in seeds:
+        cfg = rp.ReplayConfig(seed=seed, layer_proxy=True)
+        rec = paired_replay(cfg, dev, log_fn, f"layer proxy seed {seed}")
+        out["per_seed"][str(seed)] = rec
+        reds.append(rec["p99_itl_reduction_pct"])
+    mean, lo, hi = rp.paired_ci(reds)
+    out["p99_itl_reduction_vs_uncapped"] = {
+        "mean_pct": round(mean, 2), "ci95_pct": None if lo is None else [round(lo, 2), round(hi, 2)]}
+    out["overlap_20_req_s"] = paired_replay(rp.ReplayConfig(seed=seeds[0], rate_per_s=20.0,
+                                                            layer_proxy=True),
+                                            dev, log_fn, "layer proxy 20 req/s")
+    out["note"] = ("per layer: Q, K, V projections (hidden 1024), append + attention, output "
+                   "projection, MLP gate/up and down (3072), one layer timed, clock x28")
+    return out
+
+
+# The paper's workload shapes (Sec. 4.2): prompt / output tokens.
+VARIANTS = {"chat": (1024, 128), "rag": (8192, 256), "agent": (16384, 256),
+            "decode_heavy": (256, 1024)}
+
+
+def run_variant_replays(dev, seed, rate, n_requests, log_fn):
+    """Each of the paper's workload shapes as a replay with the layer proxy,
+    open-loop Poisson arrivals at the paper's rate, paired uncapped vs DLFP with
+    the paper's cap constants (c_initial 3072, c_min 1024, c_max 6144, Sec. 3.1)."""
+    from paper_2609_38386_amd import replay as rp
+    out = {}
+    for name, (prompt, outl) in VARIANTS.items():
+        cfg = rp.ReplayConfig(seed=seed, n_requests=n_requests, rate_per_s=rate,
+                              prompt_lo=prompt, prompt_hi=prompt, out_len=outl,
+                              layer_proxy=True, c_initial=3072, c_min=1024, c_max=6144)
+        out[name] = paired_replay(cfg, dev, log_fn, f"variant {name}")
+        out[name]["prompt_tokens"], out[name]["output_tokens"] = prompt, outl
+    out["note"] = (f"{n_requests} requests at {rate} req/s, seed {seed}, layer proxy, "
+                   "one layer timed, clock x28, caps 1024..6144 from c_initial 3072")
+    return out
+
+
 # ----------------------------------------------------------------------------- CPU baseline
 
 def cpu_baseline(dev, seconds, p=512, c=32):
@@ -776,6 +865,8 @@ def main():
         replay = run_replays(dev, seeds, logf)
         replay["overlap_20_req_s"] = run_overlap_replay(dev, seeds[0], 20.0, logf)
         replay["root_cause"] = run_root_cause_replays(dev, seeds[0], (2.0, 20.0), logf)
+        replay["layer_proxy"] = run_layer_proxy_replays(dev, seeds, logf)
+        replay["variants"] = run_variant_replays(dev, seeds[0], 1.0, args.variant_requests, logf)
     if any(errors.values()):
         print(f"bench.py: the workspace error word is set after the timed launches: {errors} "
               "(1 = a block id outside the pool, 2 = a wait for the append records ran out); "

@@ -311,6 +311,19 @@ int dlfp_workspace_init(void* workspace, size_t workspace_bytes, hipStream_t str
  * dlfp_append_attention_mixed stopped waiting for the append records. */
 int dlfp_workspace_error(const void* workspace, int32_t* host_error, hipStream_t stream);
 
+/* Dense projection for the full-iteration latency of Eq. 1 (the linear
+ * layers whose cost grows with the prefill chunk p_t, Sec. 2.1):
+ *   out[i][j] = sum_l x[i][l] * w[j][l],  i < m, j < n, l < k
+ * x: device bf16, row i at x + i * ldx (ldx >= k, a multiple of 8, x 16-byte
+ * aligned); w: device bf16 [n][k] (one row per output feature, as a linear
+ * layer's weight is stored), 16-byte aligned; out: device, row i at
+ * out + i * ldo (ldo >= n, a multiple of 4), out_dtype 0 = bf16 (8-byte
+ * aligned), 1 = fp32 (16-byte aligned).  fp32 accumulation.  n must be a
+ * multiple of 128 and k of 64 (DLFP_EUNSUPPORTED otherwise); m = 0 launches
+ * nothing.  Errors: DLFP_EINVAL, DLFP_EUNSUPPORTED, DLFP_EHIP. */
+int dlfp_linear_bf16(int32_t m, int32_t n, int32_t k, const void* x, int32_t ldx, const void* w,
+                     void* out, int32_t ldo, int32_t out_dtype, hipStream_t stream);
+
 /* Proportional prefill-cap controller, Eq. 2 (Sec. 3.1):
  *   cap <- clamp(quantum * floor(cap * target / observed / quantum), c_min, c_max)
  * applied after each guarded cycle (at least one decoder and a prefill shared

@@ -18,7 +18,8 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB_PATH = os.path.join(HERE, "libdlfp.so")
 ARCH = "gfx950"
 
-SOURCES = ["dlfp_host.cpp", "kv_append.hip", "attention_mixed.hip", "stream_hold.hip"]
+SOURCES = ["dlfp_host.cpp", "dlfp_timer.cpp", "kv_append.hip", "attention_mixed.hip", "stream_hold.hip",
+           "linear.hip"]
 
 # Packed FP32 instructions are kept out of device code.
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]

@@ -68,6 +68,7 @@ class dlfp_controller(ctypes.Structure):
 
 EXPORTS = ["dlfp_build_varlen_meta", "dlfp_kv_append", "dlfp_attention_mixed",
            "dlfp_append_attention_mixed", "dlfp_append_attention_mixed_static",
+           "dlfp_linear_bf16",
            "dlfp_workspace_init", "dlfp_workspace_error", "dlfp_controller_init",
            "dlfp_controller_step", "dlfp_timer_create", "dlfp_timer_destroy", "dlfp_timer_start",
            "dlfp_timer_stop", "dlfp_timer_elapsed_ms", "dlfp_stream_hold", "dlfp_status_string",
@@ -103,6 +104,7 @@ def lib():
                                                      ctypes.POINTER(dlfp_meta), vp, vp, i32, i32,
                                                      vp, vp, vp, vp, vp, ctypes.c_float, vp, i32,
                                                      vp]
+    L.dlfp_linear_bf16.argtypes = [i32, i32, i32, vp, i32, vp, vp, i32, i32, vp]
     L.dlfp_workspace_init.argtypes = [vp, sz, vp]
     L.dlfp_workspace_error.argtypes = [vp, _P32, vp]
     L.dlfp_controller_init.argtypes = [ctypes.POINTER(dlfp_controller), ctypes.c_double, i32, i32,
@@ -261,6 +263,22 @@ def dlfp_append_attention_mixed_static(dims: dlfp_dims, meta: Meta, d_work, d_bl
         _dptr(v_new), _dptr(k_cache), _dptr(v_cache), float(scale), _dptr(out), out_dtype,
         _stream(stream))
     _check(st, "dlfp_append_attention_mixed_static")
+
+
+def dlfp_linear_bf16(x, w, out, stream=None) -> None:
+    """out[i][j] = sum_l x[i][l] w[j][l]; x: bf16 [m][k] (rows may be strided),
+    w: bf16 [n][k], out: bf16 or float32 [m][n] (rows may be strided)."""
+    import torch
+    m, k = int(x.shape[0]), int(x.shape[1])
+    n = int(w.shape[0])
+    if int(w.shape[1]) != k or tuple(out.shape) != (m, n):
+        raise ValueError("shapes disagree")
+    if x.stride(1) != 1 or w.stride(1) != 1 or out.stride(1) != 1 or not w.is_contiguous():
+        raise ValueError("rows must be contiguous")
+    out_dtype = {torch.bfloat16: 0, torch.float32: 1}[out.dtype]
+    st = lib().dlfp_linear_bf16(m, n, k, _dptr(x), int(x.stride(0)), _dptr(w), _dptr(out),
+                                int(out.stride(0)), out_dtype, _stream(stream))
+    _check(st, "dlfp_linear_bf16")
 
 
 def dlfp_workspace_init(workspace, stream=None) -> None:

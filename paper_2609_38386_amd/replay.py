@@ -108,6 +108,13 @@ class ReplayConfig:
     # call, batch formation plus the executor's preparation of its launches).
     pipeline: Optional[str] = None
     host_ms: Optional[float] = None
+    # Full-iteration proxy (Eq. 1's linear term): the timed layer also runs the
+    # layer's projections around the attention -- query, key and value from the
+    # hidden states, the output projection, the MLP's gate/up and down -- with
+    # Qwen3-0.6B's sizes (hidden 1024, MLP 3072), as libdlfp matrix products.
+    layer_proxy: bool = False
+    hidden: int = 1024
+    mlp: int = 3072
 
     @property
     def max_blocks(self) -> int:
@@ -395,6 +402,22 @@ class GpuExecutor:
         for t in (self.q, self.k, self.v):
             t.normal_(generator=gen)
         self.out = torch.empty_like(self.q)
+        self.proxy = cfg.layer_proxy
+        if self.proxy:
+            # weights N(0, 1/fan_in) in bf16, [out features][in features]
+            def weight(n_out, n_in):
+                w = torch.empty((n_out, n_in), dtype=torch.float32, device=device)
+                return (w.normal_(generator=gen) / math.sqrt(n_in)).to(torch.bfloat16)
+            hq, hkv, hid = cfg.num_q_heads * 128, cfg.num_kv_heads * 128, cfg.hidden
+            self.w_q, self.w_k, self.w_v = weight(hq, hid), weight(hkv, hid), weight(hkv, hid)
+            self.w_o = weight(hid, hq)
+            self.w_gu, self.w_d = weight(2 * cfg.mlp, hid), weight(hid, cfg.mlp)
+            self.x = torch.empty((rows, hid), dtype=torch.bfloat16, device=device)
+            self.x.normal_(generator=gen)
+            self.y = torch.empty((rows, hid), dtype=torch.bfloat16, device=device)
+            self.gu = torch.empty((rows, 2 * cfg.mlp), dtype=torch.bfloat16, device=device)
+            self.y2 = torch.empty_like(self.y)
+            self.mlp = cfg.mlp
         self.stage = rt.StagedBatch(self.dims, cfg.max_seqs + 1, rows, 65536, device)
         bt_cap = (cfg.max_seqs + 1) * cfg.max_blocks
         self.bt_host = torch.empty(bt_cap, dtype=torch.int32, pin_memory=True)
@@ -402,7 +425,8 @@ class GpuExecutor:
         self.ws = rt.Workspace(device, 64 << 20)
         self.timer = D.Timer()
         self.scale = 1.0 / math.sqrt(128)
-        self.hold_us = 150
+        # the host enqueues the layer's launches while the stream idles
+        self.hold_us = 400 if self.proxy else 150
         self.last_host_ms = 0.0
 
     def __call__(self, q_len: np.ndarray, kv_len: np.ndarray, bt: np.ndarray) -> float:
@@ -421,9 +445,18 @@ class GpuExecutor:
         self.last_host_ms = (time.perf_counter() - t0) * 1e3
         D.dlfp_stream_hold(self.hold_us)
         self.timer.start()
+        if self.proxy:
+            x = self.x[:T]
+            D.dlfp_linear_bf16(x, self.w_q, self.q[:T].view(T, -1))
+            D.dlfp_linear_bf16(x, self.w_k, self.k[:T].view(T, -1))
+            D.dlfp_linear_bf16(x, self.w_v, self.v[:T].view(T, -1))
         D.dlfp_append_attention_mixed(self.dims, st.meta, st.d_work, d_bt, self.q[:T],
                                       self.k[:T], self.v[:T], self.pool.k, self.pool.v,
                                       self.scale, self.out[:T], ws)
+        if self.proxy:
+            D.dlfp_linear_bf16(self.out[:T].view(T, -1), self.w_o, self.y[:T])
+            D.dlfp_linear_bf16(self.y[:T], self.w_gu, self.gu[:T])
+            D.dlfp_linear_bf16(self.gu[:T, :self.mlp], self.w_d, self.y2[:T])
         self.timer.stop()
         return self.timer.elapsed_ms()
 

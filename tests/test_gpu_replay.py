@@ -47,3 +47,29 @@ def test_gpu_replay_uncapped_and_dlfp():
     got = [it["limit"] for it in trace2[1:]]
     assert got == want
     assert len(set(got)) > 2   # the cap moved
+
+
+def test_gpu_replay_with_the_layer_proxy():
+    """With the layer's projections timed beside the attention (Eq. 1's linear
+    term) the iteration latency grows with the prefill chunk, and the
+    completion-timed controller's decisions still match the oracle's."""
+    import numpy as np
+    assert torch.cuda.is_available()
+    dev = torch.device("cuda:0")
+    cfg = rp.ReplayConfig(seed=803, n_requests=10, rate_per_s=400.0, prompt_hi=4096, out_len=16,
+                          layer_proxy=True)
+    ex = rp.GpuExecutor(cfg, dev)
+    trace = []
+    base = rp.run_replay(cfg, rp.Policy(rp.Policy.UNCAPPED), ex, trace=trace)
+    assert base["reconciled"]
+    pts = [(it["p_t"], it["layer_ms"]) for it in trace if it["p_t"] > 0]
+    p = np.asarray([x[0] for x in pts], dtype=np.float64)
+    ms = np.asarray([x[1] for x in pts])
+    assert len(pts) >= 4 and np.corrcoef(p, ms)[0, 1] > 0.8
+    dec_only = sorted(it["layer_ms"] for it in trace if it["decoders"] > 0 and it["p_t"] == 0)
+    target = 1.2 * dec_only[len(dec_only) // 2]
+    trace2 = []
+    dl = rp.run_replay(cfg, rp.Policy(rp.Policy.DLFP, target_ms=target, cfg=cfg), ex,
+                       trace=trace2)
+    assert dl["reconciled"]
+    assert [it["limit"] for it in trace2[1:]] == expected_limits(trace2, cfg, target)
