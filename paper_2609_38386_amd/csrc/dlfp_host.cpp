@@ -1,8 +1,7 @@
 // Host half of libdlfp: packed-batch metadata and work list, the Eq. 2
-// controller, completion timers, status strings.  Device launches live in
-// kv_append.hip and attention_mixed.hip.
-#include <hip/hip_runtime.h>
-
+// controller, status strings.  Plain C++ (no HIP calls), so it also builds
+// with a host compiler and its sanitizers.  Device launches live in the .hip
+// sources; the completion timers in dlfp_timer.cpp.
 #include <algorithm>
 #include <cmath>
 #include <cstdint>
@@ -532,54 +531,6 @@ int dlfp_controller_step(dlfp_controller* ctrl, int32_t num_decoding_next,
   } else {
     *next_cap = ctrl->cap;
   }
-  return DLFP_OK;
-}
-
-struct dlfp_timer_s {
-  hipEvent_t start, stop;
-};
-
-int dlfp_timer_create(dlfp_timer* timer) {
-  if (!timer) return DLFP_EINVAL;
-  dlfp_timer t = new (std::nothrow) dlfp_timer_s;
-  if (!t) return DLFP_EINVAL;
-  if (hipEventCreate(&t->start) != hipSuccess) {
-    delete t;
-    return DLFP_EHIP;
-  }
-  if (hipEventCreate(&t->stop) != hipSuccess) {
-    (void)hipEventDestroy(t->start);
-    delete t;
-    return DLFP_EHIP;
-  }
-  *timer = t;
-  return DLFP_OK;
-}
-
-int dlfp_timer_destroy(dlfp_timer timer) {
-  if (!timer) return DLFP_EINVAL;
-  const bool ok = hipEventDestroy(timer->start) == hipSuccess &&
-                  hipEventDestroy(timer->stop) == hipSuccess;
-  delete timer;
-  return ok ? DLFP_OK : DLFP_EHIP;
-}
-
-int dlfp_timer_start(dlfp_timer timer, hipStream_t stream) {
-  if (!timer) return DLFP_EINVAL;
-  return hipEventRecord(timer->start, stream) == hipSuccess ? DLFP_OK : DLFP_EHIP;
-}
-
-int dlfp_timer_stop(dlfp_timer timer, hipStream_t stream) {
-  if (!timer) return DLFP_EINVAL;
-  return hipEventRecord(timer->stop, stream) == hipSuccess ? DLFP_OK : DLFP_EHIP;
-}
-
-int dlfp_timer_elapsed_ms(dlfp_timer timer, double* ms) {
-  if (!timer || !ms) return DLFP_EINVAL;
-  if (hipEventSynchronize(timer->stop) != hipSuccess) return DLFP_EHIP;
-  float f = 0.f;
-  if (hipEventElapsedTime(&f, timer->start, timer->stop) != hipSuccess) return DLFP_EHIP;
-  *ms = f;
   return DLFP_OK;
 }
 
