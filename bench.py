@@ -58,6 +58,9 @@ def parse_args():
                     help="seeds of the closed-loop replay (comma list, or 'none')")
     ap.add_argument("--variant-requests", type=int, default=24,
                     help="requests per workload-variant replay")
+    ap.add_argument("--tuning", default=None,
+                    help="work-list policy overrides for every sweep (the dlfp_tuning fields, "
+                         "comma-separated; 0 = automatic)")
     ap.add_argument("--quiet", action="store_true")
     ap.add_argument("--two-launch", action="store_true",
                     help="append with dlfp_kv_append, then dlfp_attention_mixed (instead of "
@@ -108,7 +111,7 @@ def append_work(hkv, num_tokens):
 # ----------------------------------------------------------------------------- sweep harness
 
 class Sweep:
-    def __init__(self, cfg, dev, n_pools, layers, seed_offset=0, fused=True):
+    def __init__(self, cfg, dev, n_pools, layers, seed_offset=0, fused=True, tuning=None):
         import torch
         from paper_2609_38386_amd import dlfp as D
         from paper_2609_38386_amd import runtime as rt
@@ -153,7 +156,7 @@ class Sweep:
         max_tok = max(cfg.chunks) + self.n
         self.out = torch.empty((max_tok, self.hq, 128), dtype=torch.bfloat16, device=dev)
         # two staging slots: the next iteration's metadata is built while one runs
-        self.stages = [rt.StagedBatch(self.dims, self.n + 1, max_tok, 1 << 17, dev)
+        self.stages = [rt.StagedBatch(self.dims, self.n + 1, max_tok, 1 << 17, dev, tuning)
                        for _ in range(2)]
         self.stage = self.stages[0]
         self.ws = rt.Workspace(dev, 64 << 20)
@@ -309,7 +312,8 @@ def record_quarter(cfg, p, c):
     return c % 4 == 3
 
 
-def run_sweep(cfg, dev, log_fn, n_pools, layers, steps, warmup, record, fused=True):
+def run_sweep(cfg, dev, log_fn, n_pools, layers, steps, warmup, record, fused=True,
+              tuning=None):
     """Time `steps` full chunk-size sweeps of `cfg` after `warmup` untimed ones.
 
     Per iteration: metadata of the next iteration built on the host while the
@@ -320,7 +324,7 @@ def run_sweep(cfg, dev, log_fn, n_pools, layers, steps, warmup, record, fused=Tr
     import torch
     from paper_2609_38386_amd import dlfp as D
     t0 = time.time()
-    sw = Sweep(cfg, dev, n_pools=n_pools, layers=layers, fused=fused)
+    sw = Sweep(cfg, dev, n_pools=n_pools, layers=layers, fused=fused, tuning=tuning)
     log_fn(f"{cfg.name}: setup {time.time() - t0:.1f}s: {n_pools} pools x {sw.num_blocks} blocks")
     # decode-only latency of the first iteration sets the controller target (1.2x)
     dec_ms = [sw.iteration(cfg.chunks[0], 0, prefill=False, record=False)[0] for _ in range(3)]
@@ -698,6 +702,76 @@ def run_variant_replays(dev, seed, rate, n_requests, log_fn):
     return out
 
 
+def measure_ceilings(dev, log_fn):
+    """Achievable ceilings from libdlfp_probe.so, timed with HIP events (median of
+    5 launches): HBM reads of random 8 KiB pieces (a decode page pair) and of a
+    contiguous stream from a 4 GiB buffer, at 1, 2 or 4 pieces in flight per
+    wavefront and 8 or 16 wavefronts per CU; bf16 MFMA with 4 accumulator chains
+    per wavefront at 8 and 16 wavefronts per CU."""
+    import ctypes
+    import torch
+    path = os.path.join(ROOT, "paper_2609_38386_amd", "libdlfp_probe.so")
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with `python -m paper_2609_38386_amd.build`")
+    L = ctypes.CDLL(path)
+    vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    L.dlfp_probe_hbm_read.argtypes = [vp, i64, vp, i32, i32, i32, i32, vp, vp]
+    L.dlfp_probe_mfma.argtypes = [i32, i32, vp, vp]
+    stream = torch.cuda.current_stream()
+    sh = ctypes.c_void_p(int(stream.cuda_stream))
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+
+    def timed(fn, reps=5):
+        fn()
+        out = []
+        for _ in range(reps):
+            ev[0].record(stream)
+            fn()
+            ev[1].record(stream)
+            ev[1].synchronize()
+            out.append(ev[0].elapsed_time(ev[1]) * 1e-3)
+        return float(np.median(out))
+
+    piece, buf_bytes = 8192, 4 << 30
+    buf = torch.empty(buf_bytes, dtype=torch.uint8, device=dev).fill_(7)
+    n_pieces = buf_bytes // piece
+    g = torch.Generator(device=dev)
+    g.manual_seed(5)
+    hbm = {}
+    for waves_per_cu in (8, 16):
+        waves = 256 * waves_per_cu
+        per_wave = (1 << 30) // piece // waves           # 1 GiB per launch
+        rand = torch.randint(0, n_pieces, (waves * per_wave,), generator=g, device=dev,
+                             dtype=torch.int32)
+        seq = torch.arange(waves * per_wave, device=dev, dtype=torch.int32)
+        sink = torch.empty(waves * 64, dtype=torch.int32, device=dev)
+        for name, idx in (("random", rand), ("stream", seq)):
+            for inflight in (1, 2, 4):
+                assert per_wave % inflight == 0 and int(idx.max()) < n_pieces
+                t = timed(lambda: L.dlfp_probe_hbm_read(
+                    vp(buf.data_ptr()), buf_bytes, vp(idx.data_ptr()), waves, per_wave, piece,
+                    inflight, vp(sink.data_ptr()), sh))
+                hbm[f"{name}_8KiB_{waves_per_cu}w_{inflight}inflight"] = round(
+                    waves * per_wave * piece / t / 1e9, 1)
+    del buf
+    mfma = {}
+    iters = 4096
+    for waves_per_cu in (8, 16):
+        wgs = 256 * waves_per_cu // 4
+        sink = torch.empty(wgs * 256, dtype=torch.float32, device=dev)
+        t = timed(lambda: L.dlfp_probe_mfma(wgs, iters, vp(sink.data_ptr()), sh))
+        mfma[f"{waves_per_cu}w"] = round(wgs * 4 * iters * 4 * 32768 / t / 1e12, 1)
+    torch.cuda.synchronize()
+    best_rand = max(v for k, v in hbm.items() if k.startswith("random"))
+    best_stream = max(v for k, v in hbm.items() if k.startswith("stream"))
+    log_fn(f"ceilings: HBM random 8 KiB {best_rand} GB/s, stream {best_stream} GB/s, "
+           f"MFMA bf16 {max(mfma.values())} TFLOP/s")
+    return {"hbm_random_8KiB_GBps": best_rand, "hbm_stream_GBps": best_stream,
+            "mfma_bf16_TFLOPs": max(mfma.values()), "hbm_GBps_by_config": hbm,
+            "mfma_TFLOPs_by_waves_per_cu": mfma,
+            "note": "libdlfp_probe.so, HIP events, median of 5 launches of 1 GiB (HBM)"}
+
+
 # ----------------------------------------------------------------------------- CPU baseline
 
 def cpu_baseline(dev, seconds, p=512, c=32):
@@ -835,10 +909,19 @@ def main():
     logf = lambda *a: log(args, *a)  # noqa: E731
     fused = not args.two_launch
     cfg = wl.qwen3_32b_config()
+    tuning = None
+    if args.tuning:
+        from paper_2609_38386_amd import dlfp as D
+        tuning = D.dlfp_tuning(*[int(x) for x in args.tuning.split(",")])
     r = run_sweep(cfg, dev, logf, n_pools=1, layers=1, steps=args.steps, warmup=args.warmup,
-                  record=record_all, fused=fused)
+                  record=record_all, fused=fused, tuning=tuning)
     logf(f"headline done: {r['wall']:.2f}s for {args.steps} steps")
     errors = {"qwen3-32b": r["workspace_error"]}
+    ceilings = None
+    if not args.headline_only:
+        ceilings = measure_ceilings(dev, logf)
+        r["roofline"]["frac_of_measured_ceiling"] = round(
+            r["roofline"]["achieved"] / ceilings["hbm_random_8KiB_GBps"], 4)
     if fused:
         r["roofline"]["traffic"] = profiled_traffic()
     cpu = None
@@ -855,7 +938,7 @@ def main():
         else:                      # each pool is far larger than the cache
             pools, layers, steps, rec = 2, 2, args.other_steps, record_all
         o = run_sweep(ocfg, dev, logf, n_pools=pools, layers=layers, steps=steps, warmup=1,
-                      record=rec, fused=fused)
+                      record=rec, fused=fused, tuning=tuning)
         extras[name] = other_shape(name, ocfg, o, layers, pools)
         errors[name] = o["workspace_error"]
         logf(f"{name} done: {o['tokens'] / o['wall']:.0f} tok/s")
@@ -888,6 +971,7 @@ def main():
                    "tokens_per_step": r["tokens"] // args.steps},
         "roofline": r["roofline"],
         "cpu_baseline": cpu,
+        "ceilings": ceilings,
         "latency_vs_pt": r["latency"],
         "shares": r["shares"],
         "controller": {"target_ms": round(r["target_ms"], 4),

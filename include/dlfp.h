@@ -124,7 +124,13 @@ typedef struct {
  * workgroup slots the prefill units leave (several queue rounds), or the
  * split that fits one round and best evens the decode workgroups over the
  * CUs, whichever an estimate of the launch time favours; a range longer than
- * its split is cut into equal parts. */
+ * its split is cut into equal parts.  Grid layout: when a launch has decode
+ * units and more prefill units than compute units, one prefill unit per
+ * compute unit leads the grid, then the decode workgroups (up to one per
+ * compute unit), then the other prefill units, so that the memory-bound decode
+ * share runs beside the matrix-core-bound prefill share from the start instead
+ * of after it.  Decode page depth: two pages in flight in a launch without
+ * prefill units, one beside them. */
 typedef struct {
   int32_t decode_split_tokens;   /* keys per decode unit; 0 = auto, else a multiple of 16,
                                     at most DLFP_MAX_DECODE_UNIT_KEYS */
@@ -135,6 +141,11 @@ typedef struct {
                                     0 = DLFP_DEFAULT_RESIDENT_WAVES */
   int32_t prefill_tile_tokens;   /* prompt tokens per prefill unit; 0 = auto, else at most
                                     DLFP_TILE_ROWS / g */
+  int32_t prefill_lead_units;    /* grid layout of a launch with both shares: the number of
+                                    prefill units placed before the first decode workgroups
+                                    (the rest follow them); 0 = auto, -1 = all of them */
+  int32_t decode_pages_in_flight;/* pages a decode wavefront keeps in flight beside its
+                                    current one: 0 = auto, 1 or 2 */
 } dlfp_tuning;
 
 /* 256 compute units x 8 resident wavefronts (two 256-thread workgroups per CU). */
@@ -158,6 +169,9 @@ typedef struct {
   int64_t workspace_bytes;    /* device workspace the attention launch needs */
   int32_t num_append;         /* append records stored after the units (see below) */
   int32_t num_waiting_units;  /* prefill units that read pages the append records write */
+  int32_t prefill_lead_units; /* grid layout chosen (see dlfp_tuning); num_prefill_units
+                                 when every prefill unit comes first */
+  int32_t decode_pages_in_flight;  /* decode page depth chosen: 1 or 2 */
 } dlfp_meta;
 
 /* Work unit fields (int32 index into one DLFP_WORK_INTS record). */

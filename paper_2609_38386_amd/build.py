@@ -34,12 +34,25 @@ def _hipcc() -> str:
     raise RuntimeError("hipcc not found; the HIP library cannot be built")
 
 
+PROBE_SOURCES = ["probes.hip"]
+PROBE_LIB_PATH = os.path.join(HERE, "libdlfp_probe.so")
+
+
+def build_probes(verbose: bool = False) -> str:
+    """libdlfp_probe.so: the achievable-ceiling probes (measurement only)."""
+    return _build(PROBE_SOURCES, PROBE_LIB_PATH, verbose, 1)
+
+
 def build_library(verbose: bool = False, jobs: int = 3) -> str:
+    return _build(SOURCES, LIB_PATH, verbose, jobs)
+
+
+def _build(sources, lib_path, verbose: bool, jobs: int) -> str:
     hipcc = _hipcc()
     tmp = tempfile.mkdtemp(prefix="dlfp_build_")
     try:
         objs, procs = [], []
-        for src in SOURCES:
+        for src in sources:
             obj = os.path.join(tmp, src + ".o")
             lang = ["-x", "hip"]
             cmd = [hipcc, *COMMON, *DEVICE_FLAGS, *lang, "-c", os.path.join(CSRC, src), "-o", obj]
@@ -51,15 +64,15 @@ def build_library(verbose: bool = False, jobs: int = 3) -> str:
             if len(procs) >= jobs:
                 _drain(procs, verbose)
         _drain(procs, verbose)
-        out_tmp = LIB_PATH + ".tmp"
+        out_tmp = lib_path + ".tmp"
         cmd = [hipcc, "-shared", f"--offload-arch={ARCH}", *objs, "-o", out_tmp]
         if verbose:
             print(" ".join(cmd), flush=True)
         r = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
         if r.returncode != 0:
             raise RuntimeError("link failed:\n" + r.stdout)
-        os.replace(out_tmp, LIB_PATH)
-        return LIB_PATH
+        os.replace(out_tmp, lib_path)
+        return lib_path
     finally:
         shutil.rmtree(tmp, ignore_errors=True)
 
@@ -79,3 +92,4 @@ def _drain(procs, verbose):
 if __name__ == "__main__":
     path = build_library(verbose="-v" in sys.argv)
     print(path)
+    print(build_probes(verbose="-v" in sys.argv))

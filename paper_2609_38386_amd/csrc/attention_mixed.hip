@@ -99,6 +99,9 @@ struct Args {
   int32_t out_f32;
   int32_t decode_waves;  // wavefronts of the decode workgroups of this launch
   int32_t decode_static; // decode units handed out by position, the rest by queue
+  int32_t lead;          // prefill workgroups before the first decode workgroup
+  int32_t decode_lead;   // decode workgroups before the remaining prefill ones
+  int32_t deep;          // decode wavefronts keep two pages in flight
   float scale_log2;      // softmax scale * log2(e)
   // Append launches only: this iteration's keys and values [tokens][hkv][128],
   // the leading workgroups that write the append records stored after the
@@ -942,7 +945,7 @@ __device__ int decode_unit(const Args& a, const int32_t* it_g, char* wl, bool ta
   // wait longer for their loads (measured 3.6-5.5% longer iterations for
   // chunks of 64-256 tokens).  A block id outside the pool is replaced by
   // block 0 after raising the error word.
-  const bool deep = a.num_prefill == 0;
+  const bool deep = a.deep != 0;
   const int p_begin = kb / PAGE, p_end = (ke + PAGE - 1) / PAGE;
   const int npages = p_end - p_begin;
   uint32_t kofs[4], vofs[4];
@@ -1263,7 +1266,7 @@ __device__ int decode_unit_mfma(const Args& a, const int32_t* it_g, char* wl, bo
   const int32_t* bt = a.block_table + (int64_t)s * a.max_blocks;
   int32_t* ptab = reinterpret_cast<int32_t*>(wl + 2 * DEC_PAGE_SLOT + 16 * 16 * 2);
 
-  const bool deep = a.num_prefill == 0;
+  const bool deep = a.deep != 0;
   const int p_begin = kb / PAGE, p_end = (ke + PAGE - 1) / PAGE;
   const int npages = p_end - p_begin;
   uint32_t kofs[4], vofs[4];
@@ -1591,8 +1594,22 @@ __global__ __launch_bounds__(THREADS, 2) void attention_mixed_kernel(Args a) {
     }
     b -= a.app_wgs;
   }
-  if (b < a.num_prefill) {
-    const int u = xcd_remap(b, a.num_prefill);
+  // Grid: `lead` prefill workgroups, `decode_lead` decode workgroups, the
+  // other prefill workgroups, the other decode workgroups.  The i-th prefill
+  // workgroup takes unit xcd_remap(i): decode_lead is a multiple of 8, so the
+  // i-th prefill workgroup runs on XCD i % 8 either way.
+  const int np = a.num_prefill, L = a.lead, DL = a.decode_lead;
+  int pi = -1, d = -1;
+  if (b < L)
+    pi = b;
+  else if (b < L + DL)
+    d = b - L;
+  else if (b < np + DL)
+    pi = b - DL;
+  else
+    d = b - np;
+  if (pi >= 0) {
+    const int u = xcd_remap(pi, np);
     prefill_unit<G, APP>(a, a.work + (int64_t)u * DLFP_WORK_INTS, smem, &flag);
   } else {
     // Decode wavefront w of decode workgroup d starts with unit 4 d + w when
@@ -1614,7 +1631,7 @@ __global__ __launch_bounds__(THREADS, 2) void attention_mixed_kernel(Args a) {
                                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       return uniform(__shfl(nt, 0));
     };
-    int t = (b - a.num_prefill) * 4 + wave;
+    int t = d * 4 + wave;
     if (queue && t >= a.decode_static) t = ticket();
     while (t < ndec) {
       // In queue mode the unit takes the next ticket itself near its end.
@@ -1700,6 +1717,9 @@ int launch_mixed(const dlfp_dims* dims, const dlfp_meta* meta, const int32_t* d_
               meta->num_waiting_units > meta->num_prefill_units))
     return DLFP_EINVAL;
   if (meta->num_units == 0) return DLFP_OK;
+  if (meta->prefill_lead_units < 0 || meta->prefill_lead_units > meta->num_prefill_units ||
+      (meta->decode_pages_in_flight != 1 && meta->decode_pages_in_flight != 2))
+    return DLFP_EINVAL;
   if (!d_work || !d_block_table || !q || !k_cache || !v_cache || !out || !workspace)
     return DLFP_EINVAL;
   if (app && !v_new) return DLFP_EINVAL;
@@ -1758,6 +1778,16 @@ int launch_mixed(const dlfp_dims* dims, const dlfp_meta* meta, const int32_t* d_
   const int slots = ahead < 2 * cus ? std::max(2 * cus - ahead, 64) : 2 * cus;
   a.decode_waves = 4 * decode_wgs;
   a.decode_static = std::min(decode_units, 4 * std::min(decode_wgs, slots));
+  a.lead = meta->num_prefill_units;
+  a.decode_lead = 0;
+  a.deep = meta->decode_pages_in_flight == 2;
+  if (meta->prefill_lead_units < meta->num_prefill_units && decode_wgs >= 8) {
+    // the leading decode workgroups are resident from the start and take their
+    // units by position; the ones after the other prefill units take tickets
+    a.lead = meta->prefill_lead_units;
+    a.decode_lead = std::min(decode_wgs, cus) / 8 * 8;
+    a.decode_static = std::min(decode_units, 4 * a.decode_lead);
+  }
   const int grid = a.app_wgs + meta->num_prefill_units + decode_wgs;
   (void)hipGetLastError();
   hipError_t e;

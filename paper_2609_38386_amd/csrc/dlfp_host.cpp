@@ -79,8 +79,10 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
   if (!meta || num_seqs < 0) return DLFP_EINVAL;
   if (num_seqs > 0 && (!q_len || !kv_len || !block_table || max_blocks <= 0)) return DLFP_EINVAL;
   if (num_blocks < 0) return DLFP_EINVAL;
-  dlfp_tuning tn = {0, 0, 0, 0};
+  dlfp_tuning tn = {0, 0, 0, 0, 0, 0};
   if (tuning) tn = *tuning;
+  if (tn.prefill_lead_units < -1) return DLFP_EINVAL;
+  if (tn.decode_pages_in_flight < 0 || tn.decode_pages_in_flight > 2) return DLFP_EINVAL;
   if (tn.decode_split_tokens < 0 || tn.decode_split_tokens % DLFP_PAGE_SIZE ||
       tn.decode_split_tokens > DLFP_MAX_DECODE_UNIT_KEYS)
     return DLFP_EINVAL;
@@ -468,6 +470,25 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
   meta->workspace_bytes = std::max<int64_t>(off * 4, partial_base_bytes);
   meta->num_append = (int32_t)appends.size();
   meta->num_waiting_units = (int32_t)waiting;
+  // Grid layout: with more prefill units than compute units, one per compute
+  // unit leads and the decode workgroups follow, so the two shares run side by
+  // side from the start (a compute unit with one prefill unit keeps about 90% of
+  // the prefill rate of one with two).
+  const int64_t n_dec_units = (int64_t)units.size() - num_prefill;
+  const int64_t cus = std::max<int64_t>(1, resident / 8);
+  int64_t lead = num_prefill;
+  if (tn.prefill_lead_units > 0)
+    lead = std::min<int64_t>(tn.prefill_lead_units, num_prefill);
+  else if (tn.prefill_lead_units == 0 && n_dec_units > 0 && num_prefill > cus)
+    lead = cus;
+  meta->prefill_lead_units = (int32_t)lead;
+  // Decode page depth: two pages in flight without a prefill share; beside
+  // one, one page (deeper decode queues delay the prefill tiles' loads; on the
+  // Qwen3-32B sweep a second page gained nothing at p_t <= 1024 and lost 3-5%
+  // at larger chunks).
+  const int depth = tn.decode_pages_in_flight ? tn.decode_pages_in_flight
+                                              : (num_prefill == 0 ? 2 : 1);
+  meta->decode_pages_in_flight = depth;
   if (meta->cap_seqs < num_seqs || meta->cap_tokens < tokens || meta->cap_work < records)
     return DLFP_ENOSPC;
   if ((num_seqs > 0 && (!meta->cu_q || !meta->q_pos0)) || (tokens > 0 && !meta->slot_mapping) ||

@@ -43,7 +43,9 @@ class dlfp_dims(ctypes.Structure):
 
 class dlfp_tuning(ctypes.Structure):
     _fields_ = [("decode_split_tokens", ctypes.c_int32), ("prefill_split_tokens", ctypes.c_int32),
-                ("target_units", ctypes.c_int32), ("prefill_tile_tokens", ctypes.c_int32)]
+                ("target_units", ctypes.c_int32), ("prefill_tile_tokens", ctypes.c_int32),
+                ("prefill_lead_units", ctypes.c_int32),
+                ("decode_pages_in_flight", ctypes.c_int32)]
 
 
 _P32 = ctypes.POINTER(ctypes.c_int32)
@@ -57,7 +59,9 @@ class dlfp_meta(ctypes.Structure):
                 ("num_units", ctypes.c_int32), ("num_prefill_units", ctypes.c_int32),
                 ("num_groups", ctypes.c_int32), ("decode_split_tokens", ctypes.c_int32),
                 ("prefill_split_tokens", ctypes.c_int32), ("workspace_bytes", ctypes.c_int64),
-                ("num_append", ctypes.c_int32), ("num_waiting_units", ctypes.c_int32)]
+                ("num_append", ctypes.c_int32), ("num_waiting_units", ctypes.c_int32),
+                ("prefill_lead_units", ctypes.c_int32),
+                ("decode_pages_in_flight", ctypes.c_int32)]
 
 
 class dlfp_controller(ctypes.Structure):

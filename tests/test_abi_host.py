@@ -228,3 +228,46 @@ def test_stream_hold_rejects_out_of_range_durations_before_any_launch():
         with pytest.raises(D.DlfpError) as e:
             D.dlfp_stream_hold(us, stream=0)
         assert e.value.status == -1
+
+
+def test_grid_layout_and_decode_depth_policy():
+    """Launches with both shares and more prefill units than compute units lead with
+    one prefill unit per compute unit; otherwise every prefill unit comes first.
+    Decode-only launches keep two pages in flight; the overrides are honoured."""
+    dims = D.make_dims(64, 8)
+    cfg = wl.qwen3_32b_config()
+    pages = cfg.pages_per_seq()
+    nb = int(sum(pages))
+    bt_all = wl.block_tables(cfg.seed, pages, nb)
+    for p, c, dec, pre in [(8192, 3, True, True), (512, 5, True, True), (8192, 3, False, True),
+                           (512, 0, True, False)]:
+        its = [x for x in cfg.iteration(p, c) if (x[1] > 1 and pre) or (x[1] == 1 and dec)]
+        ql = [x[1] for x in its]
+        kl = [x[2] for x in its]
+        bt = bt_all[[x[0] for x in its]]
+        m = D.dlfp_build_varlen_meta(dims, ql, kl, bt, nb)
+        if dec and pre and m.num_prefill_units > 256:
+            assert m.prefill_lead_units == 256
+        else:
+            assert m.prefill_lead_units == m.num_prefill_units
+        assert m.decode_pages_in_flight == (2 if m.num_prefill_units == 0 else
+                                            m.decode_pages_in_flight)
+        assert m.decode_pages_in_flight in (1, 2)
+        forced = D.dlfp_build_varlen_meta(dims, ql, kl, bt, nb,
+                                          D.dlfp_tuning(0, 0, 0, 0, -1, 1))
+        assert forced.prefill_lead_units == forced.num_prefill_units
+        assert forced.decode_pages_in_flight == 1
+    with pytest.raises(D.DlfpError):
+        D.dlfp_build_varlen_meta(dims, ql, kl, bt, nb, D.dlfp_tuning(0, 0, 0, 0, 0, 3))
+
+
+def test_probe_library_exports_its_declared_symbols():
+    import ctypes
+    txt = open(os.path.join(ROOT, "include", "dlfp_probe.h")).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    declared = sorted(set(re.findall(r"\bint\s+(dlfp_probe_\w+)\s*\(", txt)))
+    assert declared == ["dlfp_probe_hbm_read", "dlfp_probe_mfma"]
+    path = os.path.join(ROOT, "paper_2609_38386_amd", "libdlfp_probe.so")
+    L = ctypes.CDLL(path)
+    for name in declared:
+        assert hasattr(L, name), name
