@@ -1229,7 +1229,7 @@ __device__ int decode_unit(const Args& a, const int32_t* it_g, char* wl, bool ta
 
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
 
-// Decode unit for g >= 4 query heads per KV head.  The unit's g heads are the
+// Decode unit for g >= 2 query heads per KV head.  The unit's g heads are the
 // columns of 16x16 matrix products (padded to 16 with zero queries): per page,
 // the scores are S^T = K Q^T (four v_mfma_f32_16x16x32_bf16 over the 128
 // dims) and the output advances by O^T += V^T P^T (eight
@@ -1252,7 +1252,7 @@ typedef short s16x4_t __attribute__((ext_vector_type(4)));
 // decode_unit.
 template <int G, bool APP>
 __device__ int decode_unit_mfma(const Args& a, const int32_t* it_g, char* wl, bool take_ticket) {
-  static_assert(G >= 4 && G <= 16, "heads must fit the 16 columns");
+  static_assert(G >= 2 && G <= 16, "heads must fit the 16 columns");
   const int lane = threadIdx.x & 63;
   const int col = lane & 15, gq = lane >> 4;
   const record_ptr it = as_record(it_g);
@@ -1637,7 +1637,7 @@ __global__ __launch_bounds__(THREADS, 2) void attention_mixed_kernel(Args a) {
       // In queue mode the unit takes the next ticket itself near its end.
       const int32_t* rec = a.work + (int64_t)(a.num_prefill + t) * DLFP_WORK_INTS;
       int pending;
-      if constexpr (G >= 4)
+      if constexpr (G >= 2)
         pending = decode_unit_mfma<G, APP>(a, rec, wl, queue);
       else
         pending = decode_unit<G, APP>(a, rec, wl, queue);
