@@ -523,6 +523,7 @@ def run_replays(dev, seeds, log_fn):
                 red = 100.0 * (base["itl_p99_ms"] - r["itl_p99_ms"]) / base["itl_p99_ms"]
                 rec[name]["p99_itl_reduction_pct"] = round(red, 2)
                 reductions[name].append(red)
+        rec["retimed_iterations"] = ex.retimed
         out["per_seed"][str(seed)] = rec
         log_fn(f"replay seed {seed}: {time.time() - t0:.1f}s, p99 ITL uncapped "
                f"{base['itl_p99_ms']:.3f} ms, dlfp {runs['dlfp']['itl_p99_ms']:.3f} ms, "
@@ -567,6 +568,7 @@ def run_overlap_replay(dev, seed, rate, log_fn):
                                        if caps else None)}
     for name, r in (("uncapped", base), ("dlfp", dl), ("dlfp_lag1", lag)):
         out[name] = {k: (round(r[k], 4) if isinstance(r[k], float) else r[k]) for k in keys}
+    out["retimed_iterations"] = ex.retimed
     log_fn(f"overlap replay {rate} req/s: {time.time() - t0:.1f}s, controlled L/T p50 "
            f"{dl['controlled_L_over_T_p50']}, within 5% {dl['controlled_within_5pct']}")
     del ex
@@ -606,6 +608,7 @@ def run_root_cause_replays(dev, seed, rates, log_fn):
             for name, r in runs.items():
                 rec[name] = {k: (round(r[k], 4) if isinstance(r[k], float) else r[k])
                              for k in keys}
+            rec["retimed_iterations"] = ex.retimed
             out[f"{pipe}_{rate:g}_req_s"] = rec
             log_fn(f"root-cause replay {pipe} {rate} req/s: {time.time() - t0:.1f}s, p99 ITL "
                    + ", ".join(f"{n} {r['itl_p99_ms']:.3f}" for n, r in runs.items()))
@@ -650,6 +653,7 @@ def paired_replay(cfg, dev, log_fn, label):
         rec["guarded_caps"] = {"p10": int(np.percentile(caps, 10)), "p50": int(np.median(caps)),
                                "p90": int(np.percentile(caps, 90)),
                                "at_c_min": round(float(np.mean(caps == cfg.c_min)), 4)}
+    rec["retimed_iterations"] = ex.retimed
     log_fn(f"{label}: {time.time() - t0:.1f}s, p99 ITL {base['itl_p99_ms']:.3f} -> "
            f"{dl['itl_p99_ms']:.3f} ms, guarded {dl['guarded_iterations']}")
     del ex

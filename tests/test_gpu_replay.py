@@ -73,3 +73,29 @@ def test_gpu_replay_with_the_layer_proxy():
                        trace=trace2)
     assert dl["reconciled"]
     assert [it["limit"] for it in trace2[1:]] == expected_limits(trace2, cfg, target)
+
+
+def test_gpu_retimed_layer_leaves_the_same_state():
+    """An iteration whose enqueue outlasts the stream hold is timed a second
+    time; its launches are idempotent, so the pages and outputs after a replay
+    in which every iteration is timed twice (a 1 us hold) equal, bit for bit,
+    those of a replay timed once per iteration.  Uncapped decisions do not
+    depend on the measured latencies, so both replays run the same batches."""
+    assert torch.cuda.is_available()
+    dev = torch.device("cuda:0")
+    cfg = rp.ReplayConfig(seed=804, n_requests=5, rate_per_s=400.0, prompt_hi=1536, out_len=6,
+                          layer_proxy=True)
+    once, twice = rp.GpuExecutor(cfg, dev), rp.GpuExecutor(cfg, dev)
+    twice.hold_us = 1
+    t1, t2 = [], []
+    r1 = rp.run_replay(cfg, rp.Policy(rp.Policy.UNCAPPED), once, trace=t1)
+    r2 = rp.run_replay(cfg, rp.Policy(rp.Policy.UNCAPPED), twice, trace=t2)
+    assert r1["reconciled"] and r2["reconciled"]
+    assert [(x["p_t"], x["decoders"]) for x in t1] == [(x["p_t"], x["decoders"]) for x in t2]
+    assert twice.retimed == len(t2)
+    assert all(x["layer_ms"] > 0.0 for x in t2)
+    torch.cuda.synchronize()
+    rows = max(x["p_t"] + x["decoders"] for x in t1)   # rows ever written
+    for a, b in ((once.pool.k, twice.pool.k), (once.pool.v, twice.pool.v),
+                 (once.out[:rows], twice.out[:rows]), (once.y2[:rows], twice.y2[:rows])):
+        assert torch.equal(a.view(torch.int16), b.view(torch.int16))
