@@ -710,8 +710,10 @@ def measure_ceilings(dev, log_fn):
     """Achievable ceilings from libdlfp_probe.so, timed with HIP events (median of
     5 launches): HBM reads of random 8 KiB pieces (a decode page pair) and of a
     contiguous stream from a 4 GiB buffer, at 1, 2 or 4 pieces in flight per
-    wavefront and 8 or 16 wavefronts per CU; bf16 MFMA with 4 accumulator chains
-    per wavefront at 8 and 16 wavefronts per CU."""
+    wavefront and 8 or 16 wavefronts per CU, with default caching and with
+    non-temporal loads (as the decode share reads its pages); bf16 MFMA with 4
+    accumulator chains per wavefront at 8 and 16 wavefronts per CU.  The HBM
+    ceilings are the best over every configuration."""
     import ctypes
     import torch
     path = os.path.join(ROOT, "paper_2609_38386_amd", "libdlfp_probe.so")
@@ -719,7 +721,7 @@ def measure_ceilings(dev, log_fn):
         raise RuntimeError(f"{path} is missing: build it with `python -m paper_2609_38386_amd.build`")
     L = ctypes.CDLL(path)
     vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
-    L.dlfp_probe_hbm_read.argtypes = [vp, i64, vp, i32, i32, i32, i32, vp, vp]
+    L.dlfp_probe_hbm_read.argtypes = [vp, i64, vp, i32, i32, i32, i32, i32, vp, vp]
     L.dlfp_probe_mfma.argtypes = [i32, i32, vp, vp]
     stream = torch.cuda.current_stream()
     sh = ctypes.c_void_p(int(stream.cuda_stream))
@@ -750,13 +752,15 @@ def measure_ceilings(dev, log_fn):
         seq = torch.arange(waves * per_wave, device=dev, dtype=torch.int32)
         sink = torch.empty(waves * 64, dtype=torch.int32, device=dev)
         for name, idx in (("random", rand), ("stream", seq)):
-            for inflight in (1, 2, 4):
-                assert per_wave % inflight == 0 and int(idx.max()) < n_pieces
-                t = timed(lambda: L.dlfp_probe_hbm_read(
-                    vp(buf.data_ptr()), buf_bytes, vp(idx.data_ptr()), waves, per_wave, piece,
-                    inflight, vp(sink.data_ptr()), sh))
-                hbm[f"{name}_8KiB_{waves_per_cu}w_{inflight}inflight"] = round(
-                    waves * per_wave * piece / t / 1e9, 1)
+            for nt in (0, 1):
+                for inflight in (1, 2, 4):
+                    assert per_wave % inflight == 0 and int(idx.max()) < n_pieces
+                    t = timed(lambda: L.dlfp_probe_hbm_read(
+                        vp(buf.data_ptr()), buf_bytes, vp(idx.data_ptr()), waves, per_wave,
+                        piece, inflight, nt, vp(sink.data_ptr()), sh))
+                    mode = "_nt" if nt else ""
+                    hbm[f"{name}_8KiB{mode}_{waves_per_cu}w_{inflight}inflight"] = round(
+                        waves * per_wave * piece / t / 1e9, 1)
     del buf
     mfma = {}
     iters = 4096
@@ -767,10 +771,14 @@ def measure_ceilings(dev, log_fn):
         mfma[f"{waves_per_cu}w"] = round(wgs * 4 * iters * 4 * 32768 / t / 1e12, 1)
     torch.cuda.synchronize()
     best_rand = max(v for k, v in hbm.items() if k.startswith("random"))
+    best_rand_cached = max(v for k, v in hbm.items() if k.startswith("random_8KiB_")
+                           and "_nt_" not in k)
     best_stream = max(v for k, v in hbm.items() if k.startswith("stream"))
-    log_fn(f"ceilings: HBM random 8 KiB {best_rand} GB/s, stream {best_stream} GB/s, "
-           f"MFMA bf16 {max(mfma.values())} TFLOP/s")
-    return {"hbm_random_8KiB_GBps": best_rand, "hbm_stream_GBps": best_stream,
+    log_fn(f"ceilings: HBM random 8 KiB {best_rand} GB/s ({best_rand_cached} with default "
+           f"caching), stream {best_stream} GB/s, MFMA bf16 {max(mfma.values())} TFLOP/s")
+    return {"hbm_random_8KiB_GBps": best_rand,
+            "hbm_random_8KiB_default_caching_GBps": best_rand_cached,
+            "hbm_stream_GBps": best_stream,
             "mfma_bf16_TFLOPs": max(mfma.values()), "hbm_GBps_by_config": hbm,
             "mfma_TFLOPs_by_waves_per_cu": mfma,
             "note": "libdlfp_probe.so, HIP events, median of 5 launches of 1 GiB (HBM)"}

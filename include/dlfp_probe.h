@@ -24,10 +24,11 @@ extern "C" {
  * of the device buffer `buf` (`buf_bytes` bytes): wavefront w reads pieces
  * pieces[w * per_wave + p] (device int32, piece indices, clamped into the
  * buffer), `inflight` (1, 2 or 4) pieces outstanding at a time, with 16-byte
- * loads.  sink: device uint32 [waves * 64], one folded word per lane. */
+ * loads, marked non-temporal when `nontemporal` is 1 (0: default caching).
+ * sink: device uint32 [waves * 64], one folded word per lane. */
 int dlfp_probe_hbm_read(const void* buf, int64_t buf_bytes, const int32_t* pieces, int32_t waves,
-                        int32_t per_wave, int32_t piece_bytes, int32_t inflight, uint32_t* sink,
-                        hipStream_t stream);
+                        int32_t per_wave, int32_t piece_bytes, int32_t inflight,
+                        int32_t nontemporal, uint32_t* sink, hipStream_t stream);
 
 /* `workgroups` 256-thread workgroups, each wavefront issuing `iters` x 4
  * independent v_mfma_f32_32x32x16_bf16 (32768 flop each).  sink: device

@@ -4,9 +4,9 @@
 //
 // HBM: each wavefront reads whole pieces (for example the 8 KiB a decode unit
 // reads per page: a 4 KiB key page and a 4 KiB value page) at given piece
-// indices of a large buffer with 16-byte loads, `inflight` pieces outstanding
-// at a time, and folds them into one word per lane (written once, so no load is
-// dead).  MFMA: back-to-back v_mfma_f32_32x32x16_bf16 in independent
+// indices of a large buffer with 16-byte loads (optionally non-temporal, as
+// the decode share reads its pages), `inflight` pieces outstanding at a time,
+// and folds them into one word per lane (written once, so no load is dead).  MFMA: back-to-back v_mfma_f32_32x32x16_bf16 in independent
 // accumulator chains per wavefront.
 #include <hip/hip_runtime.h>
 
@@ -23,7 +23,7 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 // Piece p of wavefront w is pieces[w * per_wave + p]; a piece of `bytes`
 // bytes is read as bytes / 1024 rounds of one 16-byte load per lane, with
 // INFLIGHT pieces issued before any is consumed.
-template <int INFLIGHT>
+template <int INFLIGHT, bool NT>
 __global__ __launch_bounds__(256) void hbm_read_kernel(const char* buf, int64_t buf_pieces,
                                                        const int32_t* pieces, int32_t per_wave,
                                                        int32_t piece_bytes, uint32_t* sink) {
@@ -41,7 +41,10 @@ __global__ __launch_bounds__(256) void hbm_read_kernel(const char* buf, int64_t 
       const char* base = buf + idx * piece_bytes;
 #pragma unroll
       for (int r = 0; r < 8; ++r)
-        if (r < rounds) v[i][r] = *reinterpret_cast<const u32x4_t*>(base + r * 1024 + 16 * lane);
+        if (r < rounds) {
+          const u32x4_t* src = reinterpret_cast<const u32x4_t*>(base + r * 1024 + 16 * lane);
+          v[i][r] = NT ? __builtin_nontemporal_load(src) : *src;
+        }
     }
 #pragma unroll
     for (int i = 0; i < INFLIGHT; ++i)
@@ -73,24 +76,38 @@ __global__ __launch_bounds__(256) void mfma_kernel(int32_t iters, float* sink) {
   sink[(int64_t)blockIdx.x * 256 + threadIdx.x] = s;
 }
 
+template <bool NT>
+int launch_hbm_read(const char* b, int64_t n, const int32_t* pieces, int32_t waves,
+                    int32_t per_wave, int32_t piece_bytes, int32_t inflight, uint32_t* sink,
+                    hipStream_t stream) {
+  const dim3 grid(waves / 4);
+  switch (inflight) {
+    case 1: hbm_read_kernel<1, NT><<<grid, 256, 0, stream>>>(b, n, pieces, per_wave, piece_bytes, sink); break;
+    case 2: hbm_read_kernel<2, NT><<<grid, 256, 0, stream>>>(b, n, pieces, per_wave, piece_bytes, sink); break;
+    case 4: hbm_read_kernel<4, NT><<<grid, 256, 0, stream>>>(b, n, pieces, per_wave, piece_bytes, sink); break;
+    default: return -1;
+  }
+  return 0;
+}
+
 }  // namespace
 
 extern "C" int dlfp_probe_hbm_read(const void* buf, int64_t buf_bytes, const int32_t* pieces,
                                    int32_t waves, int32_t per_wave, int32_t piece_bytes,
-                                   int32_t inflight, uint32_t* sink, hipStream_t stream) {
+                                   int32_t inflight, int32_t nontemporal, uint32_t* sink,
+                                   hipStream_t stream) {
   if (!buf || !pieces || !sink || waves <= 0 || waves % 4 || per_wave <= 0) return -1;
+  if (nontemporal != 0 && nontemporal != 1) return -1;
+  if (inflight != 1 && inflight != 2 && inflight != 4) return -1;
   if (piece_bytes < 1024 || piece_bytes > 8192 || piece_bytes % 1024) return -1;
   if (buf_bytes < piece_bytes) return -1;
-  const dim3 grid(waves / 4);
   (void)hipGetLastError();
   const char* b = static_cast<const char*>(buf);
   const int64_t n = buf_bytes / piece_bytes;
-  switch (inflight) {
-    case 1: hbm_read_kernel<1><<<grid, 256, 0, stream>>>(b, n, pieces, per_wave, piece_bytes, sink); break;
-    case 2: hbm_read_kernel<2><<<grid, 256, 0, stream>>>(b, n, pieces, per_wave, piece_bytes, sink); break;
-    case 4: hbm_read_kernel<4><<<grid, 256, 0, stream>>>(b, n, pieces, per_wave, piece_bytes, sink); break;
-    default: return -1;
-  }
+  if (nontemporal)
+    launch_hbm_read<true>(b, n, pieces, waves, per_wave, piece_bytes, inflight, sink, stream);
+  else
+    launch_hbm_read<false>(b, n, pieces, waves, per_wave, piece_bytes, inflight, sink, stream);
   return hipGetLastError() == hipSuccess ? 0 : -4;
 }
 
