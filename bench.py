@@ -161,8 +161,11 @@ class Sweep:
         self.stage = self.stages[0]
         self.ws = rt.Workspace(dev, 64 << 20)
         self.timer = D.Timer()
-        self.ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-                   for _ in range(layers)]
+        # two sets of per-layer launch events, so that one iteration's can be read
+        # while the next iteration runs
+        self.ev_sets = [[(torch.cuda.Event(enable_timing=True),
+                          torch.cuda.Event(enable_timing=True)) for _ in range(layers)]
+                        for _ in range(2)]
         self.stream = torch.cuda.current_stream()
         self.scale = 1.0 / math.sqrt(128)
         self.L = D.lib()
@@ -201,10 +204,11 @@ class Sweep:
                 "qkv": (qa[lo:lo + T], ka[lo:lo + T], va[lo:lo + T]),
                 "guarded": bool(prefill and decoders), "decoders": decoders}
 
-    def launch(self, pr, record=True):
+    def launch(self, pr, record=True, evset=0):
         """Enqueue the layers of a prepared iteration between the completion timer's
-        events; with `record`, HIP events also bracket every attention launch (the
-        one-launch append + attention, or the attention alone with two launches)."""
+        events; with `record`, HIP events (of set `evset`) also bracket every
+        attention launch (the one-launch append + attention, or the attention alone
+        with two launches)."""
         D = self.D
         st, T, bt, d_bt = pr["st"], pr["T"], pr["bt"], pr["d_bt"]
         q, k, v = pr["qkv"]
@@ -220,12 +224,13 @@ class Sweep:
                     ct.c_size_t(ws.numel()), stream)
         kv_new = (vp(k.data_ptr()), vp(v.data_ptr()))
         L = self.L
+        ev = self.ev_sets[evset]
         self.timer.start(self.stream)
         for layer in range(self.layers):
             pk, pv = self.pool_ptrs[layer % len(self.pools)]
             if self.fused:
                 if record:
-                    self.ev[layer][0].record(self.stream)
+                    ev[layer][0].record(self.stream)
                 rc = L.dlfp_append_attention_mixed(*att_head, *kv_new, pk, pv, *att_tail)
                 if rc:
                     D._check(rc, "dlfp_append_attention_mixed")
@@ -234,23 +239,32 @@ class Sweep:
                 if rc:
                     D._check(rc, "dlfp_kv_append")
                 if record:
-                    self.ev[layer][0].record(self.stream)
+                    ev[layer][0].record(self.stream)
                 rc = L.dlfp_attention_mixed(*att_head, pk, pv, *att_tail)
                 if rc:
                     D._check(rc, "dlfp_attention_mixed")
             if record:
-                self.ev[layer][1].record(self.stream)
+                ev[layer][1].record(self.stream)
         self.timer.stop(self.stream)
         pr["record"] = record
+        pr["evset"] = evset
 
-    def finish(self, pr, ctrl=None):
+    def finish(self, pr, ctrl=None, events=True):
         """Wait for the iteration (completion timing), step the controller from the
-        measured latency; returns (device ms, [attention ms per layer], q_len, kv_len)."""
+        measured latency; returns (device ms, [attention ms per layer], q_len, kv_len).
+        With `events` False the per-launch events are left to `attention_ms`."""
         ms = self.timer.elapsed_ms()
-        attn = [a.elapsed_time(b) for a, b in self.ev] if pr["record"] else []
         if ctrl is not None:
             self.D.dlfp_controller_step(ctrl, self.n if pr["decoders"] else 0, pr["guarded"], ms)
+        attn = self.attention_ms(pr) if events else None
         return ms, attn, pr["q_len"], pr["kv_len"]
+
+    def attention_ms(self, pr):
+        """Per-layer launch times of a finished iteration (valid until its event set
+        is recorded again, two launches later)."""
+        if not pr["record"]:
+            return []
+        return [a.elapsed_time(b) for a, b in self.ev_sets[pr["evset"]]]
 
     def iteration(self, p, c, ctrl=None, decoders=True, prefill=True, record=True):
         """Prepare, launch and finish one mixed iteration."""
@@ -332,31 +346,43 @@ def run_sweep(cfg, dev, log_fn, n_pools, layers, steps, warmup, record, fused=Tr
     ctrl = D.dlfp_controller_init(target, 2048, 32, max(4096, max(cfg.chunks)), 128)
     iters = [(p, c) for p in cfg.chunks for c in range(cfg.prompt_len // p)]
 
+    def account(stats, p, c, pr, ms, cap):
+        """The benchmark's own bookkeeping of a finished iteration (run while the
+        next iteration is on the device)."""
+        ql, kl = pr["q_len"], pr["kv_len"]
+        s = stats.setdefault(p, {"iter_ms": [], "attn_ms": 0.0, "attn_launch_ms": [],
+                                 "bytes": 0, "flops": 0, "tokens": 0, "caps": [],
+                                 "recorded": 0, "by_chunk": {}})
+        s["iter_ms"].append(ms)
+        s["by_chunk"].setdefault(c, []).append(ms)
+        s["tokens"] += int(ql.sum())
+        s["caps"].append(cap)
+        if pr["record"]:
+            attn = sw.attention_ms(pr)
+            s["recorded"] += 1
+            s["attn_ms"] += sum(attn)
+            s["attn_launch_ms"] += list(attn)
+            db, pb, df, pf = attn_work(sw.hq, sw.hkv, ql, kl)
+            ab = append_work(sw.hkv, int(ql.sum())) if sw.fused else 0
+            s["bytes"] += (db + pb + ab) * layers
+            s["flops"] += (df + pf) * layers
+
     def step(stats):
+        # Per iteration: launch, account for the previous iteration while this one
+        # runs, build the next iteration's metadata, then wait for completion and
+        # step the controller (Eq. 2) before the next launch.
         pr = sw.prepare(*iters[0], slot=0)
+        pending = None
         for i, (p, c) in enumerate(iters):
-            rec = record(cfg, p, c)
-            sw.launch(pr, record=rec)
+            sw.launch(pr, record=record(cfg, p, c), evset=i & 1)
+            if pending is not None and stats is not None:
+                account(stats, *pending)
             nxt = sw.prepare(*iters[i + 1], slot=(i + 1) & 1) if i + 1 < len(iters) else None
-            ms, attn, ql, kl = sw.finish(pr, ctrl)
+            ms = sw.finish(pr, ctrl, events=False)[0]
+            pending = (p, c, pr, ms, ctrl.cap)
             pr = nxt
-            if stats is None:
-                continue
-            s = stats.setdefault(p, {"iter_ms": [], "attn_ms": 0.0, "attn_launch_ms": [],
-                                     "bytes": 0, "flops": 0, "tokens": 0, "caps": [],
-                                     "recorded": 0, "by_chunk": {}})
-            s["iter_ms"].append(ms)
-            s["by_chunk"].setdefault(c, []).append(ms)
-            s["tokens"] += int(ql.sum())
-            s["caps"].append(ctrl.cap)
-            if rec:
-                s["recorded"] += 1
-                s["attn_ms"] += sum(attn)
-                s["attn_launch_ms"] += list(attn)
-                db, pb, df, pf = attn_work(sw.hq, sw.hkv, ql, kl)
-                ab = append_work(sw.hkv, int(ql.sum())) if sw.fused else 0
-                s["bytes"] += (db + pb + ab) * layers
-                s["flops"] += (df + pf) * layers
+        if pending is not None and stats is not None:
+            account(stats, *pending)
 
     for _ in range(warmup):
         step(None)
