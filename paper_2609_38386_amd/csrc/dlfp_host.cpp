@@ -472,8 +472,8 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
   meta->num_waiting_units = (int32_t)waiting;
   // Grid layout: with more prefill units than compute units, one per compute
   // unit leads and the decode workgroups follow, so the two shares run side by
-  // side from the start (a compute unit with one prefill unit keeps about 90% of
-  // the prefill rate of one with two).
+  // side from the start instead of the decode units running alone after the
+  // last prefill tile.
   const int64_t n_dec_units = (int64_t)units.size() - num_prefill;
   const int64_t cus = std::max<int64_t>(1, resident / 8);
   int64_t lead = num_prefill;
