@@ -462,6 +462,20 @@ def other_shape(name, cfg, r, layers, pools):
             "workspace_error": r["workspace_error"]}
 
 
+def shares_against_ceilings(shares, ceilings):
+    """Add to a shares record the fraction of the measured ceilings: the decode
+    share's rate over the random 8 KiB HBM ceiling, each prefill share's over the
+    bf16 MFMA ceiling (the matrix cores at the clock they hold under sustained
+    load, against which the 2.5 PFLOP/s rating is not reachable)."""
+    if not ceilings:
+        return shares
+    shares["decode"]["frac_of_measured_hbm_ceiling"] = round(
+        shares["decode"]["GBps"] / ceilings["hbm_random_8KiB_GBps"], 4)
+    for v in shares["prefill_last_chunk"].values():
+        v["frac_of_measured_mfma_ceiling"] = round(v["TFLOPs"] / ceilings["mfma_bf16_TFLOPs"], 4)
+    return shares
+
+
 def measure_shares(sw, cfg, min_launches=20):
     """Decode-only and prefill-only launches of the same kernel (rotating pools),
     at least ``min_launches`` of each, each timed with its own events.  Rates are
@@ -960,6 +974,7 @@ def main():
         ceilings = measure_ceilings(dev, logf)
         r["roofline"]["frac_of_measured_ceiling"] = round(
             r["roofline"]["achieved"] / ceilings["hbm_random_8KiB_GBps"], 4)
+        shares_against_ceilings(r["shares"], ceilings)
     if fused:
         r["roofline"]["traffic"] = profiled_traffic()
     cpu = None
@@ -977,6 +992,7 @@ def main():
             pools, layers, steps, rec = 2, 2, args.other_steps, record_all
         o = run_sweep(ocfg, dev, logf, n_pools=pools, layers=layers, steps=steps, warmup=1,
                       record=rec, fused=fused, tuning=tuning)
+        shares_against_ceilings(o["shares"], ceilings)
         extras[name] = other_shape(name, ocfg, o, layers, pools)
         errors[name] = o["workspace_error"]
         logf(f"{name} done: {o['tokens'] / o['wall']:.0f} tok/s")
