@@ -307,3 +307,29 @@ def test_score_spikes_far_above_the_rest(dev, ws, g):
     torch.cuda.synchronize()
     assert D.dlfp_workspace_error(ws.buf) == 0
     _compare(_to64(out), seqs, f"score spikes g={g}")
+
+
+def test_maximum_unit_sizes(dev, ws):
+    """Units at the library's limits: prefill units of exactly
+    DLFP_MAX_PREFILL_UNIT_KEYS keys in one split (their block ids fill the LDS
+    table), decode units of exactly DLFP_MAX_DECODE_UNIT_KEYS keys (a 4096-key
+    decoder whole, a 32768-key decoder in eight splits), a 4097-key context in
+    two equal splits, and a one-key decoder.  Every row against the oracle; the
+    output is NaN-filled."""
+    shape = wl.AttnShape(16, 8)
+    specs = [(16, 32768), (1, 4096), (1, 4097), (1, 32768), (1, 1)]
+    seqs = _seqs(shape, specs, seed=4242)
+    it = rt.Iteration(D.make_dims(16, 8), seqs, _pool_for(seqs), 8, dev,
+                      fill_bits=rt.BF16_NAN_BITS, tuning=D.dlfp_tuning(4096, 32768, 0))
+    m = it.batch.meta
+    pre = m.work[:m.num_prefill_units]
+    dec = m.work[m.num_prefill_units:m.num_units]
+    assert len(pre) == 8 and all(int(u[5]) - int(u[4]) == 32768 for u in pre)
+    assert int((dec[:, 5] - dec[:, 4]).max()) == 4096
+    assert int((dec[:, 5] - dec[:, 4]).min()) == 1
+    out = torch.full((m.num_tokens, 16, 128), float("nan"), dtype=torch.float32, device=dev)
+    it.run(ws, SCALE, out=out)
+    torch.cuda.synchronize()
+    assert D.dlfp_workspace_error(ws.buf) == 0
+    _compare(_to64(out), seqs, "maximum unit sizes")
+    assert not ws.buf[:D.WORKSPACE_PARTIALS].view(torch.int32).cpu().numpy().any()
