@@ -31,6 +31,11 @@
  *    DLFP_EHIP from a launch that follows another launch of the same call
  *    (only dlfp_append_attention_mixed with more than 128 append records,
  *    see there) leaves the first launch's work enqueued.
+ *  - Empty batches: a launch call given no work (num_tokens 0 for
+ *    dlfp_kv_append, a metadata with num_units 0 for the attention calls,
+ *    as dlfp_build_varlen_meta makes for num_seqs 0) checks its dims and
+ *    counts, launches nothing and returns DLFP_OK; its device pointers are
+ *    not read and may be null (an empty device tensor's address).
  *  - Ownership: the caller owns every buffer (device and host).  The library
  *    allocates no device memory and keeps no pointer after returning.
  *  - Device calls are stream-ordered and asynchronous; a device-side fault
@@ -299,9 +304,9 @@ int dlfp_append_attention_mixed(const dlfp_dims* dims, const dlfp_meta* meta,
  * copy per GPU, until the process ends; arguments otherwise as for that call
  * (the caller still passes every input and output).  The call allocates
  * nothing: no hipMalloc, no hipFree, no allocating library routine.  Its first
- * call on a device looks up the array's address on that device and zeroes its
- * header and counter region with a fill kernel on `stream`; every launch
- * leaves them zero again.  All calls on one GPU share that GPU's array:
+ * call with work on a device looks up the array's address on that device and
+ * zeroes its header and counter region with a fill kernel on `stream`; every
+ * launch leaves them zero again.  All calls on one GPU share that GPU's array:
  * calls that overlap on one GPU (on different streams, or from different
  * threads without ordering) race on it and must not be made.
  * Errors: DLFP_ENOSPC when meta->workspace_bytes exceeds

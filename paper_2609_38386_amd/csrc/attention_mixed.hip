@@ -1706,11 +1706,13 @@ hipError_t launch(const Args& a, int grid, hipStream_t stream) {
   return hipGetLastError();
 }
 
-// Validation, grid and launch shared by both entry points; k_new / v_new are
-// null for the attention-only launch.
+// Validation, grid and launch shared by the entry points; `app` selects the
+// fused append (k_new / v_new are ignored without it).  A batch without units
+// returns DLFP_OK after its counts are checked, before any pointer is.
 int launch_mixed(const dlfp_dims* dims, const dlfp_meta* meta, const int32_t* d_work,
                  const int32_t* d_block_table, int32_t max_blocks, int32_t num_blocks,
-                 const void* q, const void* k_new, const void* v_new, const void* k_cache,
+                 const void* q, bool app, const void* k_new, const void* v_new,
+                 const void* k_cache,
                  const void* v_cache, float scale, void* out, int32_t out_dtype, void* workspace,
                  size_t workspace_bytes, hipStream_t stream) {
   int g = 0;
@@ -1722,7 +1724,6 @@ int launch_mixed(const dlfp_dims* dims, const dlfp_meta* meta, const int32_t* d_
   if (meta->num_units < 0 || meta->num_prefill_units < 0 ||
       meta->num_prefill_units > meta->num_units || meta->num_groups < 0)
     return DLFP_EINVAL;
-  const bool app = k_new != nullptr;
   if (app && (meta->num_append < 0 || meta->num_waiting_units < 0 ||
               (meta->num_append > 0 && meta->num_waiting_units == 0) ||
               meta->num_waiting_units > meta->num_prefill_units))
@@ -1733,7 +1734,7 @@ int launch_mixed(const dlfp_dims* dims, const dlfp_meta* meta, const int32_t* d_
     return DLFP_EINVAL;
   if (!d_work || !d_block_table || !q || !k_cache || !v_cache || !out || !workspace)
     return DLFP_EINVAL;
-  if (app && !v_new) return DLFP_EINVAL;
+  if (app && (!k_new || !v_new)) return DLFP_EINVAL;
   if (max_blocks <= 0 || num_blocks <= 0) return DLFP_EINVAL;
   if ((int64_t)workspace_bytes < meta->workspace_bytes ||
       workspace_bytes < (size_t)DLFP_WORKSPACE_PARTIALS)
@@ -1842,8 +1843,8 @@ extern "C" int dlfp_attention_mixed(const dlfp_dims* dims, const dlfp_meta* meta
                                     const void* v_cache, float scale, void* out,
                                     int32_t out_dtype, void* workspace, size_t workspace_bytes,
                                     hipStream_t stream) {
-  return launch_mixed(dims, meta, d_work, d_block_table, max_blocks, num_blocks, q, nullptr,
-                      nullptr, k_cache, v_cache, scale, out, out_dtype, workspace,
+  return launch_mixed(dims, meta, d_work, d_block_table, max_blocks, num_blocks, q, false,
+                      nullptr, nullptr, k_cache, v_cache, scale, out, out_dtype, workspace,
                       workspace_bytes, stream);
 }
 
@@ -1854,9 +1855,8 @@ extern "C" int dlfp_append_attention_mixed(const dlfp_dims* dims, const dlfp_met
                                            void* v_cache, float scale, void* out,
                                            int32_t out_dtype, void* workspace,
                                            size_t workspace_bytes, hipStream_t stream) {
-  if (!k_new || !v_new) return DLFP_EINVAL;
-  return launch_mixed(dims, meta, d_work, d_block_table, max_blocks, num_blocks, q, k_new,
-                      v_new, k_cache, v_cache, scale, out, out_dtype, workspace,
+  return launch_mixed(dims, meta, d_work, d_block_table, max_blocks, num_blocks, q, true,
+                      k_new, v_new, k_cache, v_cache, scale, out, out_dtype, workspace,
                       workspace_bytes, stream);
 }
 
@@ -1868,14 +1868,18 @@ extern "C" int dlfp_append_attention_mixed_static(const dlfp_dims* dims, const d
                                                   const void* v_new, void* k_cache,
                                                   void* v_cache, float scale, void* out,
                                                   int32_t out_dtype, hipStream_t stream) {
-  if (!k_new || !v_new || !meta) return DLFP_EINVAL;
+  if (!meta) return DLFP_EINVAL;
   if (meta->workspace_bytes > (int64_t)DLFP_STATIC_WORKSPACE_BYTES) return DLFP_ENOSPC;
+  if (meta->num_units == 0)  // checks the counts only; no set-up, no launch
+    return launch_mixed(dims, meta, d_work, d_block_table, max_blocks, num_blocks, q, true,
+                        k_new, v_new, k_cache, v_cache, scale, out, out_dtype, nullptr, 0,
+                        stream);
   void* ws = nullptr;
   const int st = static_workspace(&ws, stream);
   if (st != DLFP_OK) return st;
-  return launch_mixed(dims, meta, d_work, d_block_table, max_blocks, num_blocks, q, k_new, v_new,
-                      k_cache, v_cache, scale, out, out_dtype, ws, DLFP_STATIC_WORKSPACE_BYTES,
-                      stream);
+  return launch_mixed(dims, meta, d_work, d_block_table, max_blocks, num_blocks, q, true, k_new,
+                      v_new, k_cache, v_cache, scale, out, out_dtype, ws,
+                      DLFP_STATIC_WORKSPACE_BYTES, stream);
 }
 
 extern "C" int dlfp_workspace_init(void* workspace, size_t workspace_bytes, hipStream_t stream) {

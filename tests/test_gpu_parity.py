@@ -247,6 +247,14 @@ def test_abi_rejects_bad_arguments(dev, ws):
         D.dlfp_attention_mixed(D.make_dims(16, 8, head_dim=64), b.meta, b.d_work,
                                b.d_block_table, it.q, it.pool.k, it.pool.v, SCALE, out, ws.buf)
     assert e.value.status == -5
+    # a batch with work needs its new keys and values: an empty (null) k_new is refused
+    nothing = torch.empty((0, 8, 128), dtype=torch.bfloat16, device=dev)
+    for k_new, v_new in ((nothing, it.v_new), (it.k_new, nothing)):
+        with pytest.raises(D.DlfpError) as e:
+            D.dlfp_append_attention_mixed(b.dims, b.meta, b.d_work, b.d_block_table, it.q,
+                                          k_new, v_new, it.pool.k, it.pool.v, SCALE, out,
+                                          ws.buf)
+        assert e.value.status == -1
 
 
 @pytest.mark.parametrize("p,chunk", [(64, 0), (64, 127), (512, 7), (2048, 0), (2048, 3)])
@@ -333,3 +341,36 @@ def test_maximum_unit_sizes(dev, ws):
     assert D.dlfp_workspace_error(ws.buf) == 0
     _compare(_to64(out), seqs, "maximum unit sizes")
     assert not ws.buf[:D.WORKSPACE_PARTIALS].view(torch.int32).cpu().numpy().any()
+
+
+def test_empty_batch_launches_nothing(dev):
+    """A batch with no sequences, every device array empty (null pointers), through
+    every launch entry point: each returns success without launching, the pool keeps
+    every bit, and the workspace header and counters stay zero."""
+    dims = D.make_dims(16, 8)
+    meta = D.dlfp_build_varlen_meta(dims, [], [], np.zeros((0, 1), np.int32), 8)
+    assert meta.num_units == 0 and meta.num_tokens == 0 and meta.num_append == 0
+    pool = rt.KVPool(8, 8, dev, fill_bits=0x7FC1)
+    before = pool.host_bits()
+    ws0 = rt.Workspace(dev, 1 << 16)
+
+    def empty(*shape, dtype=torch.bfloat16):
+        t = torch.empty(shape, dtype=dtype, device=dev)
+        assert t.data_ptr() == 0
+        return t
+
+    d_work = empty(0, D.WORK_INTS, dtype=torch.int32)
+    d_bt = empty(0, 1, dtype=torch.int32)
+    q, kv = empty(0, 16, 128), empty(0, 8, 128)
+    out = empty(0, 16, 128, dtype=torch.float32)
+    D.dlfp_kv_append(dims, kv, kv, empty(0, dtype=torch.int32), pool.k, pool.v)
+    D.dlfp_attention_mixed(dims, meta, d_work, d_bt, q, pool.k, pool.v, SCALE, out, ws0.buf)
+    D.dlfp_append_attention_mixed(dims, meta, d_work, d_bt, q, kv, kv, pool.k, pool.v, SCALE,
+                                  out, ws0.buf)
+    D.dlfp_append_attention_mixed_static(dims, meta, d_work, d_bt, q, kv, kv, pool.k, pool.v,
+                                         SCALE, out)
+    torch.cuda.synchronize()
+    assert D.dlfp_workspace_error(ws0.buf) == 0
+    assert not ws0.buf[:D.WORKSPACE_PARTIALS].cpu().numpy().any()
+    after = pool.host_bits()
+    assert np.array_equal(before[0], after[0]) and np.array_equal(before[1], after[1])
