@@ -68,6 +68,12 @@ def parse_args():
     ap.add_argument("--pmc-workload", choices=["sweep-32b", "sweep-0.6b", "shares-8b",
                                                "shares-32b"], default=None,
                     help="counter-pass workloads (see pmc_workload)")
+    ap.add_argument("--plot", default=None,
+                    help="also write a figure of latency vs p_t for every shape of the run "
+                         "to this path (PNG)")
+    ap.add_argument("--plot-from", default=None,
+                    help="draw the --plot figure from the last JSON line of this file and exit "
+                         "(no GPU needed)")
     return ap.parse_args()
 
 
@@ -899,6 +905,13 @@ def cpu_baseline(dev, seconds, p=512, c=32):
                     break
     except OSError:
         pass
+    import re
+    m = re.search(r"BLAS_INFO=([^,\s]+)", torch.__config__.show())
+    blas = m.group(1) if m else "unknown"
+    lib = [ln.strip() for ln in torch.__config__.parallel_info().splitlines()
+           if "Math Kernel Library" in ln or "OpenBLAS" in ln]
+    if lib:
+        blas = f"{blas} ({lib[0]})"
     return {"value": round(tokens / per_iter, 2), "unit": "tok/s",
             "cores": int(torch.get_num_threads()), "kind": "oracle",
             "sample": (f"float64 oracle (PyTorch CPU ops) on iteration p_t={p}, chunk {c} of the "
@@ -909,7 +922,7 @@ def cpu_baseline(dev, seconds, p=512, c=32):
             "seconds": round(time.perf_counter() - t0, 2),
             "prefill_s_per_iteration": round(t_prompt, 3),
             "decode_s_per_iteration": round(t_dec * cfg.n_decoders, 3),
-            "cpu_model": model, "nproc": os.cpu_count()}
+            "cpu_model": model, "nproc": os.cpu_count(), "blas": blas}
 
 
 # ----------------------------------------------------------------------------- main
@@ -952,8 +965,53 @@ def pmc_workload(dev, kind, fused=True):
                       "copy_bytes_each_way": 1 << 30}), flush=True)
 
 
+def plot_latency(line, path):
+    """Latency of one mixed iteration per timed layer against the prefill chunk
+    p_t, one panel per shape of a bench line: the mean over the sweep's chunk
+    iterations, the first-to-last chunk spread (their medians), the decode-only
+    iteration at p_t = 0, and the ideal-overlap bound t_lb of the same work."""
+    import matplotlib
+    matplotlib.use("Agg")
+    import matplotlib.pyplot as plt
+    panels = [("Qwen3-32B (headline), 1 layer", line["latency_vs_pt"],
+               line["controller"]["decode_only_iter_ms"], 1)]
+    for name, o in line.get("other_shapes", {}).items():
+        pretty = "Qwen3-" + name.split("-", 1)[1].upper()
+        panels.append((f"{pretty}, {o['layers_per_iteration_timed']} layers per iteration",
+                       o["latency_vs_pt"], o["decode_only_iter_ms"],
+                       o["layers_per_iteration_timed"]))
+    fig, axes = plt.subplots(1, len(panels), figsize=(5.2 * len(panels), 4.2), squeeze=False)
+    for ax, (title, lat, dec_ms, layers) in zip(axes[0], panels):
+        ps = sorted(lat, key=int)
+        x = np.arange(len(ps) + 1)
+        mean = [dec_ms * 1e3 / layers] + [lat[p]["iter_ms_mean"] * 1e3 / layers for p in ps]
+        lo = [mean[0]] + [min(lat[p]["iter_ms_first_mid_last"]) * 1e3 / layers for p in ps]
+        hi = [mean[0]] + [max(lat[p]["iter_ms_first_mid_last"]) * 1e3 / layers for p in ps]
+        ax.fill_between(x, lo, hi, alpha=0.25, label="first / last chunk (medians)")
+        ax.plot(x, mean, "o-", label="mean over the sweep's chunks")
+        ax.plot(x[1:], [lat[p]["t_lb_us"] for p in ps], "k--", lw=1,
+                label="t_lb = max(B / 8 TB/s, F / 2.5 PF)")
+        ax.set_xticks(x, ["0\n(decode\nonly)"] + ps)
+        ax.set_xlabel("prefill chunk p_t (tokens)")
+        ax.set_ylabel("attention latency per layer (us)")
+        ax.set_ylim(bottom=0)
+        ax.set_title(title, fontsize=10)
+        ax.grid(alpha=0.3)
+        ax.legend(fontsize=7, loc="upper left")
+    fig.suptitle(f"Mixed-iteration latency vs p_t on one MI355X ({line['value'] / 1e3:.1f}k "
+                 f"tokens/s headline)", fontsize=11)
+    fig.tight_layout()
+    fig.savefig(path, dpi=110)
+    plt.close(fig)
+
+
 def main():
     args = parse_args()
+    if args.plot_from:
+        with open(args.plot_from) as fh:
+            rows = [r for r in fh.read().splitlines() if r.startswith("{")]
+        plot_latency(json.loads(rows[-1]), args.plot or "latency_vs_pt.png")
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported: the library "
               "has no multi-GPU path (the hot path would shard by KV head or by sequence "
@@ -1049,6 +1107,8 @@ def main():
         "paper_context": "27.7% mean P99 ITL reduction, Qwen3-0.6B BF16, 1x A100 80GB (context only)",
     }
     print(json.dumps(line), flush=True)
+    if args.plot:
+        plot_latency(line, args.plot)
 
 
 if __name__ == "__main__":
