@@ -3,8 +3,10 @@
 Each shape runs at the sizes and in the launch configuration the benchmark
 times: automatic split policy, one launch per iteration that appends the new
 keys and values and attends (dlfp_append_attention_mixed; one iteration per
-shape runs dlfp_kv_append + dlfp_attention_mixed instead), one bf16 pool filled
-on the device by a seeded generator.
+shape runs dlfp_kv_append + dlfp_attention_mixed instead), bf16 output, one
+bf16 pool filled on the device by a seeded generator.  The extra decode-only,
+prefill-only and two-launch iterations of each shape write fp32 output, so
+both output types are compared at every shape and for both shares.
 
 Inputs.  The pool is filled once and copied to the host.  An iteration's new
 keys and values are the pool's own bits at the slots of its new tokens (slots
@@ -106,10 +108,12 @@ class FullSize:
         self.labels = []
         _log(f"{cfg.name}: pool of {self.num_blocks} blocks ready in {time.time() - t0:.1f}s")
 
-    def run(self, p, c, decoders=True, prefill=True, fused=True, all_rows=False):
+    def run(self, p, c, decoders=True, prefill=True, fused=True, all_rows=False,
+            out_dtype=torch.bfloat16):
         its = [x for x in self.cfg.iteration(p, c)
                if (x[1] > 1 and prefill) or (x[1] == 1 and decoders)]
-        label = f"{self.cfg.name} p={p} c={c} dec={decoders} pre={prefill} fused={fused}"
+        label = (f"{self.cfg.name} p={p} c={c} dec={decoders} pre={prefill} fused={fused} "
+                 f"out={str(out_dtype).split('.')[-1]}")
         ii = len(self.labels)
         self.labels.append(label)
         q_len = np.array([x[1] for x in its], dtype=np.int32)
@@ -131,7 +135,7 @@ class FullSize:
         v16[blk, :, :, vp] = NAN_BITS
         q = torch.empty((T, self.hq, 128), dtype=torch.bfloat16, device=self.dev)
         q.normal_(generator=self.gen)
-        out = torch.full((T, self.hq, 128), float("nan"), dtype=torch.float32, device=self.dev)
+        out = torch.full((T, self.hq, 128), float("nan"), dtype=out_dtype, device=self.dev)
         ws = self.ws.ensure(m.workspace_bytes)
         _log(f"{label}: {m.num_units} units ({m.num_prefill_units} prefill), "
              f"splits {m.prefill_split_tokens}/{m.decode_split_tokens}")
@@ -153,7 +157,7 @@ class FullSize:
         dec = [i for i, x in enumerate(its) if x[1] == 1]
         if dec:
             idx = torch.as_tensor(cu[dec], device=self.dev)
-            q_dec, out_dec = q.view(torch.int16)[idx].cpu(), out[idx].cpu()
+            q_dec, out_dec = q.view(torch.int16)[idx].cpu(), out[idx].float().cpu()
             for j, i in enumerate(dec):
                 sid, _, kl = its[i]
                 self.dec_rows[sid].append((ii, kl - 1, q_dec[j], out_dec[j]))
@@ -164,7 +168,7 @@ class FullSize:
                         stratified_prompt_rows(m.work, m.num_prefill_units, i, pos0))
                 r = torch.as_tensor(rows, device=self.dev) + int(cu[i])
                 self.prompt_rows.append((ii, pos0 + np.asarray(rows),
-                                         q.view(torch.int16)[r].cpu(), out[r].cpu()))
+                                         q.view(torch.int16)[r].cpu(), out[r].float().cpu()))
 
     def check(self):
         errs = {}   # (iteration, share) -> [abs errors]
@@ -195,14 +199,15 @@ class FullSize:
                 errs.setdefault((r[0], "decode"), []).append(np.abs(got[j] - want[j]).ravel())
             if d % 32 == 31:
                 _log(f"decoders 0..{d} checked, {time.time() - t0:.1f}s")
-        worst = 0.0
+        worst = {}
         for (ii, share), parts in sorted(errs.items()):
             e = np.concatenate(parts)
             mx, mean = float(e.max()), float(e.mean())
-            worst = max(worst, mx)
+            kind = self.labels[ii].rsplit("out=", 1)[1]
+            worst[kind] = max(worst.get(kind, 0.0), mx)
             assert mx <= MAX_ABS and mean <= MEAN_ABS, (self.labels[ii], share, mx, mean)
-        _log(f"{self.cfg.name}: {len(errs)} (iteration, share) pairs within bounds, "
-             f"worst |err| {worst:.2e}, {sum(len(r) for r in self.dec_rows.values())} decoder "
+        _log(f"{self.cfg.name}: {len(errs)} (iteration, share) pairs within bounds, worst |err| "
+             f"{', '.join(f'{k} output {v:.2e}' for k, v in sorted(worst.items()))}, {sum(len(r) for r in self.dec_rows.values())} decoder "
              f"rows, {sum(len(r[1]) for r in self.prompt_rows)} prompt rows")
 
 
@@ -216,9 +221,9 @@ def test_qwen3_0_6b_every_row_first_mid_last():
     for p in f.cfg.chunks:
         for c in _first_mid_last(f.cfg, p):
             f.run(p, c, all_rows=True)
-    f.run(f.cfg.chunks[0], 3, prefill=False, all_rows=True)
-    f.run(2048, 3, decoders=False, all_rows=True)
-    f.run(512, 9, fused=False, all_rows=True)
+    f.run(f.cfg.chunks[0], 3, prefill=False, all_rows=True, out_dtype=torch.float32)
+    f.run(2048, 3, decoders=False, all_rows=True, out_dtype=torch.float32)
+    f.run(512, 9, fused=False, all_rows=True, out_dtype=torch.float32)
     f.check()
 
 
@@ -227,9 +232,9 @@ def test_qwen3_8b_full_sweep():
     for p in f.cfg.chunks:
         for c in range(f.cfg.prompt_len // p):
             f.run(p, c)
-    f.run(4096, 3, decoders=False)
-    f.run(256, 5, prefill=False)
-    f.run(1024, 5, fused=False)
+    f.run(4096, 3, decoders=False, out_dtype=torch.float32)
+    f.run(256, 5, prefill=False, out_dtype=torch.float32)
+    f.run(1024, 5, fused=False, out_dtype=torch.float32)
     f.check()
 
 
@@ -238,7 +243,7 @@ def test_qwen3_32b_first_mid_last():
     for p in f.cfg.chunks:
         for c in _first_mid_last(f.cfg, p):
             f.run(p, c)
-    f.run(8192, 3, decoders=False)
-    f.run(512, 2, prefill=False)
-    f.run(2048, 7, fused=False)
+    f.run(8192, 3, decoders=False, out_dtype=torch.float32)
+    f.run(512, 2, prefill=False, out_dtype=torch.float32)
+    f.run(2048, 7, fused=False, out_dtype=torch.float32)
     f.check()
