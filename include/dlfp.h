@@ -116,20 +116,23 @@ typedef struct {
 } dlfp_dims;
 
 /* How the attention launch splits key ranges (split-K).  Zero fields pick
- * the built-in policy: prefill key ranges are cut so the prefill share offers
- * about one unit per compute unit (never below 1024 keys); a launch too
- * small to offer that many units, even counting its decode workgroups, is
+ * the built-in policy.  Prefill: a launch too small to give every compute
+ * unit a workgroup at 1024-key splits (decode workgroups counted) is
  * latency-bound and takes tiles of 32 rows (32 / g tokens) with the shortest
- * of 256, 512 or 1024-key splits that keeps its units within two per compute
- * unit; otherwise, when the launch has a decode share, the prefill takes the
- * tallest tile of 128, 64 or 32 rows whose units, at the shortest split of at
- * least 1024 keys keeping them at most one per compute unit, come within 1/16
- * of that count (32 rows when none does); the decode split is either
+ * of 256, 512 or 1024-key splits that keeps its workgroups within two per
+ * compute unit; otherwise, when the launch has a decode share, the prefill
+ * takes the tallest tile of 128, 64 or 32 rows whose units, at the shortest
+ * split of at least 1024 keys keeping them at most one per compute unit, come
+ * within 1/16 of that count (32 rows when none does); a prefill share alone
+ * takes 128-row tiles and the split (a multiple of 64 keys, at least 1024)
+ * that minimises an estimate of the launch time.  The decode split is either
  * sqrt(256 W / F) keys for W decode keys over the F wavefronts of the
  * workgroup slots the prefill units leave (several queue rounds), or the
  * split that fits one round and best evens the decode workgroups over the
  * CUs, whichever an estimate of the launch time favours; a range longer than
- * its split is cut into equal parts.  Grid layout: when a launch has decode
+ * its split is cut into equal parts, the last of them cut again into a half
+ * and two quarters when the decode queue runs one to six rounds.  Grid
+ * layout: when a launch has decode
  * units and more prefill units than compute units, one prefill unit per
  * compute unit leads the grid, then the decode workgroups (up to one per
  * compute unit), then the other prefill units, so that the memory-bound decode
