@@ -7,6 +7,7 @@ import re
 import numpy as np
 import pytest
 
+import _random_mixes as rm
 from oracle import controller as oc
 from oracle import meta as om
 from paper_2609_38386_amd import dlfp as D
@@ -106,6 +107,19 @@ def test_meta_random_mixes(seed):
     tn = D.dlfp_tuning(int(rng.choice([0, 16, 48, 128])), int(rng.choice([0, 64, 192])), 0,
                        int(rng.integers(0, 128 // g + 1)))
     _check_against_twin(D.make_dims(g * hkv, hkv), q_len, kv_len, bt, pool, tn)
+
+
+@pytest.mark.parametrize("i", range(rm.CASES))
+def test_meta_of_the_random_gpu_mixes(i):
+    """The random mixes the GPU parity test launches: the library's metadata equals
+    the twin's, so every case's work list covers exactly the visible pairs before
+    any of them runs on a device."""
+    g, hkv, specs, tn, _, _ = rm.case(i)
+    q_len, kv_len = [q for q, _ in specs], [k for _, k in specs]
+    pages = [wl.pages_for(k) for k in kv_len]
+    bt = wl.block_tables(rm.seed(i), pages, rm.pool(pages))
+    _check_against_twin(D.make_dims(g * hkv, hkv), q_len, kv_len, bt, rm.pool(pages),
+                        D.dlfp_tuning(*tn))
 
 
 def test_meta_small_prefill_share_takes_latency_tiles():

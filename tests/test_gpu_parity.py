@@ -9,6 +9,7 @@ import numpy as np
 import pytest
 import torch
 
+import _random_mixes as rm
 from oracle import attention as oa
 from oracle import paging as op
 from paper_2609_38386_amd import dlfp as D
@@ -374,3 +375,24 @@ def test_empty_batch_launches_nothing(dev):
     assert not ws0.buf[:D.WORKSPACE_PARTIALS].cpu().numpy().any()
     after = pool.host_bits()
     assert np.array_equal(before[0], after[0]) and np.array_equal(before[1], after[1])
+
+
+@pytest.mark.parametrize("i", range(rm.CASES))
+def test_random_mix(dev, ws, i):
+    """Seeded random mixes of GQA shape, decoders, prompt chunks, tuning, launch
+    form and output type (the cases whose metadata the CPU suite checks against
+    the twin): every row against the oracle, the error word clear and the
+    counters back at zero."""
+    g, hkv, specs, tn, fused, fp32_out = rm.case(i)
+    shape = wl.AttnShape(g * hkv, hkv)
+    seqs = _seqs(shape, specs, seed=rm.seed(i))
+    pages = [wl.pages_for(s.kv_len) for s in seqs]
+    print(f"random mix {i}: g={g} hkv={hkv} {len(seqs)} sequences, tuning {tn}, "
+          f"fused={fused}, fp32 output={fp32_out}", flush=True)
+    it = rt.Iteration(D.make_dims(g * hkv, hkv), seqs, rm.pool(pages), rm.seed(i), dev,
+                      fill_bits=rt.BF16_NAN_BITS, tuning=D.dlfp_tuning(*tn))
+    out = it.run(ws, SCALE, torch.float32 if fp32_out else torch.bfloat16, fused=fused)
+    torch.cuda.synchronize()
+    assert D.dlfp_workspace_error(ws.buf) == 0
+    assert not ws.buf[:D.WORKSPACE_PARTIALS].view(torch.int32).cpu().numpy().any()
+    _compare(_to64(out), seqs, f"random mix {i}")
