@@ -83,6 +83,20 @@ def test_gather_hand_example():
     assert v[17, 1, 0] == 1151 and v[19, 0, 2] == 1053
 
 
+def test_value_page_slot_order_is_the_declared_one():
+    """A value page row stores token slot t at position pi(t), pi trading slots 4-7
+    with 8-11 (bits 2 and 3 of t swapped), as the pool layout declares."""
+    assert [paging.value_position(t) for t in range(16)] == \
+        [0, 1, 2, 3, 8, 9, 10, 11, 4, 5, 6, 7, 12, 13, 14, 15]
+    assert all(paging.value_position(paging.value_position(t)) == t for t in range(16))
+    # a gather through a literal page, written without value_position
+    vc = np.zeros((1, 1, 1, 16), dtype=np.uint16)
+    vc[0, 0, 0] = [0, 1, 2, 3, 8, 9, 10, 11, 4, 5, 6, 7, 12, 13, 14, 15]
+    kc = np.zeros((1, 1, 16, 1), dtype=np.uint16)
+    _, v = paging.gather_sequence(kc, vc, np.array([0]), 16)
+    assert v[:, 0, 0].tolist() == list(range(16))
+
+
 def test_page_permutation_invariance():
     """Two different physical placements gather to the same bits, hence the same outputs."""
     shape = wl.AttnShape(4, 2)
