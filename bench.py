@@ -438,8 +438,8 @@ def run_sweep(cfg, dev, log_fn, n_pools, layers, steps, warmup, record, fused=Tr
     g = sw.hq // sw.hkv
     roofline = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None,
-                "kernel": (f"attention_mixed_kernel<{g}, true> (append + attention)" if sw.fused
-                           else f"attention_mixed_kernel<{g}, false>"),
+                "kernel": (f"attention_mixed_kernel<{g}, true, true> (append + attention)"
+                           if sw.fused else f"attention_mixed_kernel<{g}, false, true>"),
                 "launches_timed": n_launch,
                 "avg_launch_us": round(avg_launch_s * 1e6, 2),
                 "algorithmic_bytes_per_launch": int(bytes_all / n_launch),
