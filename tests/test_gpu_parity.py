@@ -318,29 +318,32 @@ def test_score_spikes_far_above_the_rest(dev, ws, g):
     _compare(_to64(out), seqs, f"score spikes g={g}")
 
 
-def test_maximum_unit_sizes(dev, ws):
+@pytest.mark.parametrize("g,hkv,fused", [(2, 8, False), (1, 4, True), (8, 2, True), (4, 1, False)])
+def test_maximum_unit_sizes(dev, ws, g, hkv, fused):
     """Units at the library's limits: prefill units of exactly
     DLFP_MAX_PREFILL_UNIT_KEYS keys in one split (their block ids fill the LDS
     table), decode units of exactly DLFP_MAX_DECODE_UNIT_KEYS keys (a 4096-key
     decoder whole, a 32768-key decoder in eight splits), a 4097-key context in
-    two equal splits, and a one-key decoder.  Every row against the oracle; the
-    output is NaN-filled."""
-    shape = wl.AttnShape(16, 8)
+    two equal splits, and a one-key decoder; for each decode path (g = 1 on the
+    VALU, g >= 2 on MFMA) and both launch forms.  Every row against the oracle;
+    the output is NaN-filled."""
+    hq = g * hkv
+    shape = wl.AttnShape(hq, hkv)
     specs = [(16, 32768), (1, 4096), (1, 4097), (1, 32768), (1, 1)]
-    seqs = _seqs(shape, specs, seed=4242)
-    it = rt.Iteration(D.make_dims(16, 8), seqs, _pool_for(seqs), 8, dev,
+    seqs = _seqs(shape, specs, seed=4242 + g)
+    it = rt.Iteration(D.make_dims(hq, hkv), seqs, _pool_for(seqs), 8, dev,
                       fill_bits=rt.BF16_NAN_BITS, tuning=D.dlfp_tuning(4096, 32768, 0))
     m = it.batch.meta
     pre = m.work[:m.num_prefill_units]
     dec = m.work[m.num_prefill_units:m.num_units]
-    assert len(pre) == 8 and all(int(u[5]) - int(u[4]) == 32768 for u in pre)
+    assert len(pre) == hkv and all(int(u[5]) - int(u[4]) == 32768 for u in pre)
     assert int((dec[:, 5] - dec[:, 4]).max()) == 4096
     assert int((dec[:, 5] - dec[:, 4]).min()) == 1
-    out = torch.full((m.num_tokens, 16, 128), float("nan"), dtype=torch.float32, device=dev)
-    it.run(ws, SCALE, out=out)
+    out = torch.full((m.num_tokens, hq, 128), float("nan"), dtype=torch.float32, device=dev)
+    it.run(ws, SCALE, out=out, fused=fused)
     torch.cuda.synchronize()
     assert D.dlfp_workspace_error(ws.buf) == 0
-    _compare(_to64(out), seqs, "maximum unit sizes")
+    _compare(_to64(out), seqs, f"maximum unit sizes g={g} hkv={hkv} fused={fused}")
     assert not ws.buf[:D.WORKSPACE_PARTIALS].view(torch.int32).cpu().numpy().any()
 
 
