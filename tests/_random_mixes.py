@@ -10,9 +10,12 @@ automatic about half the time), the one-launch or two-launch form and the
 output type.  Sequence s's pages come from wl.block_tables(seed(i), pages,
 pool(pages)), as rt.Iteration lays them out.
 """
+import os
+
 import numpy as np
 
-CASES = 24
+# Cases the tests run; DLFP_RANDOM_MIXES raises it for a longer sweep.
+CASES = int(os.environ.get("DLFP_RANDOM_MIXES", "24"))
 
 
 def seed(i):
