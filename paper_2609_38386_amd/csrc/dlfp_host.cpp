@@ -7,6 +7,7 @@
 #include <cstdint>
 #include <cstring>
 #include <limits>
+#include <memory>
 #include <vector>
 
 #include "dlfp.h"
@@ -25,6 +26,7 @@ int64_t slot_floats(int64_t rows) { return round_up(rows * (DLFP_HEAD_DIM + 2), 
 struct Unit {
   int32_t f[DLFP_WORK_INTS];
 };
+static_assert(sizeof(Unit) == DLFP_WORK_INTS * sizeof(int32_t), "work records are packed");
 
 }  // namespace
 
@@ -104,8 +106,12 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
     const int64_t pages = ceil_div(kl, DLFP_PAGE_SIZE);
     if (pages > max_blocks) return DLFP_ERANGE;
     const int32_t* row = block_table + (int64_t)s * max_blocks;
-    for (int64_t p = 0; p < pages; ++p)
-      if (row[p] < 0 || row[p] >= num_blocks) return DLFP_ERANGE;
+    int32_t lo = std::numeric_limits<int32_t>::max(), hi = std::numeric_limits<int32_t>::min();
+    for (int64_t p = 0; p < pages; ++p) {  // branch-free, so the scan vectorises
+      lo = std::min(lo, row[p]);
+      hi = std::max(hi, row[p]);
+    }
+    if (lo < 0 || hi >= num_blocks) return DLFP_ERANGE;
     if ((int64_t)num_blocks * DLFP_PAGE_SIZE > std::numeric_limits<int32_t>::max())
       return DLFP_ERANGE;
     tokens += ql;
@@ -237,8 +243,18 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
     const int64_t target = std::max<int64_t>(1, resident / 8);
     for (int rows : {DLFP_TILE_ROWS, DLFP_TILE_ROWS / 2, DLFP_TILE_ROWS / 4}) {
       const int64_t tt = std::max(1, rows / g);
-      int64_t sp = 1024;
-      while (sp < DLFP_MAX_PREFILL_UNIT_KEYS && prefill_units(tt, sp) > target) sp += 64;
+      // The shortest split of 1024 + 64 k keys keeping the units within the
+      // target (DLFP_MAX_PREFILL_UNIT_KEYS when none does), by bisection: the
+      // unit count only falls as the split grows.
+      int64_t lo = 0, hi = (DLFP_MAX_PREFILL_UNIT_KEYS - 1024) / 64;
+      while (lo < hi) {
+        const int64_t mid = (lo + hi) / 2;
+        if (prefill_units(tt, 1024 + 64 * mid) > target)
+          lo = mid + 1;
+        else
+          hi = mid;
+      }
+      const int64_t sp = 1024 + 64 * lo;
       if (prefill_units(tt, sp) * 16 >= target * 15 || rows == DLFP_TILE_ROWS / 4) {
         tile_tokens = (int)tt;
         split_p = sp;
@@ -292,8 +308,23 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
                                : resident / 4);
   }
 
-  // Build units: prefill (KV-head-major), then decode.
+  // Build units: prefill (KV-head-major), then decode.  Capacity: every key
+  // range is cut into at most ceil(range / split) parts, plus two tail pieces.
   std::vector<Unit> units;
+  {
+    int64_t bound = 0;
+    for (int s = 0; s < num_seqs; ++s) {
+      if (q_len[s] == 1) {
+        bound += hkv * (ceil_div(kv_len[s], split_d) + 2);
+        continue;
+      }
+      const int64_t pos0 = kv_len[s] - q_len[s];
+      for (int64_t t0 = 0; t0 < q_len[s]; t0 += tile_tokens)
+        bound += hkv * (ceil_div(pos0 + t0 + std::min<int64_t>(tile_tokens, q_len[s] - t0),
+                                 split_p) + 2);
+    }
+    units.reserve((size_t)bound);
+  }
   std::vector<int64_t> cu_q_of(num_seqs + 1, 0);  // packed row of each sequence's first token
   for (int s = 0; s < num_seqs; ++s) cu_q_of[s + 1] = cu_q_of[s] + q_len[s];
   int32_t groups = 0;
@@ -391,10 +422,26 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
     for (int kh = 0; kh < hkv; ++kh)
       emit(s, kh, 0, 1, kv_len[s], split_d, DLFP_PAGE_SIZE, DLFP_KIND_DECODE, decode_tail);
   }
-  // Decode wavefronts take units in list order from a queue: longest first.
-  std::stable_sort(units.begin() + num_prefill, units.end(), [](const Unit& x, const Unit& y) {
-    return x.f[DLFP_W_KVEND] - x.f[DLFP_W_KVBEGIN] > y.f[DLFP_W_KVEND] - y.f[DLFP_W_KVBEGIN];
-  });
+  // Decode wavefronts take units in list order from a queue: longest first,
+  // ties in emission order (a stable counting sort on the key count, which the
+  // split keeps within 1..DLFP_MAX_DECODE_UNIT_KEYS).
+  {
+    constexpr int32_t K = DLFP_MAX_DECODE_UNIT_KEYS;
+    const size_t first = (size_t)num_prefill, nd = units.size() - first;
+    std::vector<int32_t> start(K + 1, 0);
+    for (size_t i = first; i < units.size(); ++i) {
+      const int32_t len = units[i].f[DLFP_W_KVEND] - units[i].f[DLFP_W_KVBEGIN];
+      if (len < 1 || len > K) return DLFP_ERANGE;
+      ++start[K - len + 1];
+    }
+    for (int32_t b = 1; b <= K; ++b) start[b] += start[b - 1];
+    std::unique_ptr<Unit[]> sorted(new Unit[nd]);  // no zero fill: every slot is written
+    for (size_t i = first; i < units.size(); ++i) {
+      const int32_t len = units[i].f[DLFP_W_KVEND] - units[i].f[DLFP_W_KVBEGIN];
+      sorted[start[K - len]++] = units[i];
+    }
+    std::copy(sorted.get(), sorted.get() + nd, units.begin() + first);
+  }
   if ((int64_t)units.size() > std::numeric_limits<int32_t>::max() / DLFP_WORK_INTS)
     return DLFP_ERANGE;
   if (groups > DLFP_MAX_GROUPS) return DLFP_ERANGE;
@@ -428,6 +475,12 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
   // token).  A prefill unit waits for them when its last key lies in a page
   // from the one holding its sequence's first new token on.
   std::vector<Unit> appends;
+  {
+    int64_t n = 0;
+    for (int s = 0; s < num_seqs; ++s)
+      if (q_len[s] != 1) n += hkv * (q_len[s] / DLFP_PAGE_SIZE + 2);
+    appends.reserve((size_t)n);
+  }
   for (int s = 0; s < num_seqs; ++s) {
     if (q_len[s] == 1) continue;
     const int64_t pos0 = kv_len[s] - q_len[s];
@@ -506,11 +559,10 @@ int dlfp_build_varlen_meta(const dlfp_dims* dims, const dlfp_tuning* tuning, int
     }
     meta->cu_q[s + 1] = (int32_t)t;
   }
-  for (size_t u = 0; u < units.size(); ++u)
-    std::memcpy(meta->work + u * DLFP_WORK_INTS, units[u].f, sizeof(units[u].f));
-  for (size_t r = 0; r < appends.size(); ++r)
-    std::memcpy(meta->work + (units.size() + r) * DLFP_WORK_INTS, appends[r].f,
-                sizeof(appends[r].f));
+  if (!units.empty()) std::memcpy(meta->work, units.data(), units.size() * sizeof(Unit));
+  if (!appends.empty())
+    std::memcpy(meta->work + units.size() * DLFP_WORK_INTS, appends.data(),
+                appends.size() * sizeof(Unit));
   return DLFP_OK;
 }
 
